@@ -1,0 +1,106 @@
+/*
+ * libdyad -- the Dyad layer (arXiv 2312.06881) on AMD Instinct MI355X (gfx950).
+ *
+ * A Dyad layer replaces the dense weight W (n_out x n_in) of y = W x + b
+ * (Sec. 2.1) by the sum of two sparse components (Sec. 2.2, Eq. 1), each stored
+ * as a 3-D tensor of n_dyad blocks:
+ *   W1 = BlockDiag  [n_dyad][n_out/n_dyad][n_in/n_dyad]   (Sec. 2.2.1, Eq. 2)
+ *   W2 = BlockTrans [n_dyad][n_out/n_dyad][n_in/n_dyad]   (Sec. 2.2.2, Eq. 5-10)
+ * With D = n_dyad, bi = n_in/D, bo = n_out/D, entry W_c[i][j][k] sits in the
+ * dense W at (row, col):
+ *   W1, every variant:  (i*bo + j, i*bi + k)
+ *   W2, DYAD_IT:        (i*bo + j, k*D  + i)   input transposed   (Eq. 9-10)
+ *   W2, DYAD_OT:        (j*D  + i, i*bi + k)   output transposed  (Sec. 2.4.1, Eq. 11-13)
+ *   W2, DYAD_DT:        (j*D  + i, k*D  + i)   both               (Sec. 2.4.2, Eq. 14-16)
+ * (The paper's n_in/n_out are per-block sizes; here n_in/n_out are the full
+ * layer widths, and bi/bo the per-block ones.)
+ *
+ * Layouts: every activation is token-major and row-major: X[M][n_in],
+ * Y, H, dZ [M][n_out], dX, H_in [M][n_in]; W1, W2, dW1, dW2 as above; bias and
+ * db [n_out].  All tensors are contiguous device memory of the call's dtype,
+ * every non-NULL pointer 16-byte aligned.  Arithmetic accumulates in fp32;
+ * bf16 results are rounded to nearest even.
+ *
+ * Ownership and ordering: the caller allocates and owns every buffer, the
+ * dW workspace included; the library keeps no per-call allocation.  Every
+ * call only enqueues work on `stream` (NULL = the null stream) and returns
+ * without synchronising; results are valid once that work completes.  Outputs
+ * are overwritten, never accumulated into.
+ *
+ * Errors: each call returns DYAD_OK (0) or a negative dyad_status.  All
+ * argument checks run before any HIP call, so a rejected call touches no
+ * device state.  M == 0 is a valid, empty batch.
+ */
+#ifndef DYAD_H
+#define DYAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { DYAD_IT = 0, DYAD_OT = 1, DYAD_DT = 2 } dyad_variant; /* Sec. 2.2, 2.4 */
+typedef enum { DYAD_F32 = 0, DYAD_BF16 = 1 } dyad_dtype;
+typedef enum { DYAD_ACT_NONE = 0, DYAD_ACT_GELU = 1 } dyad_act; /* GELU(x) = x * Phi(x), erf form */
+
+typedef enum {
+    DYAD_OK = 0,
+    DYAD_ERR_INVALID_ARG = -1, /* unknown enum, size < 0 (M) or <= 0 (n_in, n_out, n_dyad), size overflow, NULL required pointer */
+    DYAD_ERR_SHAPE = -2,       /* n_in or n_out not divisible by n_dyad (the paper pads; padding is the caller's job) */
+    DYAD_ERR_ALIGN = -3,       /* a non-NULL pointer is not 16-byte aligned */
+    DYAD_ERR_DTYPE = -4,       /* unknown dtype */
+    DYAD_ERR_WORKSPACE = -5,   /* dW workspace NULL or smaller than dyad_dw_workspace_bytes() */
+    DYAD_ERR_LAUNCH = -6,      /* the HIP runtime rejected a kernel launch */
+} dyad_status;
+
+/*
+ * Forward pass, Sec. 2.2 Eq. 1: Y[m] = W X[m] + bias for every token m, with W
+ * assembled from W1, W2 by the variant's maps.  bias may be NULL (no bias).
+ * act == DYAD_ACT_GELU returns Y = GELU(W X + bias); then, when H is not NULL,
+ * H receives the pre-activation W X + bias (what dyad_backward_dx needs as
+ * H_in for the next layer).  H is ignored when act == DYAD_ACT_NONE.
+ * X, Y may be NULL when M == 0.
+ */
+int dyad_forward(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                 dyad_dtype dtype, const void *X, const void *W1, const void *W2,
+                 const void *bias, dyad_act act, void *Y, void *H, hipStream_t stream);
+
+/*
+ * Input gradient of y = W x + b (the paper gives no backward pass; this is the
+ * gradient of Eq. 1): dX[m] = W^T dZ[m], where dZ is the gradient w.r.t. this
+ * layer's linear output.  If this layer's input was X = GELU(H_in)
+ * (act_in == DYAD_ACT_GELU), dX is returned already multiplied by GELU'(H_in),
+ * i.e. it is the gradient w.r.t. H_in; H_in [M][n_in] is then required.
+ * dZ, dX may be NULL when M == 0.
+ */
+int dyad_backward_dx(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype, const void *dZ, const void *W1, const void *W2,
+                     dyad_act act_in, const void *H_in, void *dX, hipStream_t stream);
+
+/*
+ * Weight and bias gradients of Eq. 1: dW_c[i][j][k] = sum_m dZ[m][row] X[m][col]
+ * over the (row, col) the entry occupies, db[f] = sum_m dZ[m][f].  dbias may be
+ * NULL.  The sums over m are taken in a fixed order, so results are bitwise
+ * reproducible run to run.  workspace must hold dyad_dw_workspace_bytes() bytes
+ * (it may be NULL when that is 0); its contents on entry do not matter.
+ * With M == 0 the gradients are zero.
+ */
+int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype, const void *dZ, const void *X, void *dW1, void *dW2,
+                     void *dbias, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes dyad_backward_dw needs for these arguments (0 if none, or if they are invalid). */
+size_t dyad_dw_workspace_bytes(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad,
+                               int64_t M, dyad_dtype dtype);
+
+/* Static, human-readable text for a dyad_status value. */
+const char *dyad_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DYAD_H */

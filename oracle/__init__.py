@@ -62,6 +62,8 @@ def _load():
     lib.oracle_backward_dw.restype = None
     lib.oracle_backward_dw.argtypes = [ctypes.c_int, _I64, _I64, _I64, _I64,
                                        _D, _D, _D, _D, _D]
+    lib.oracle_bias_grad.restype = None
+    lib.oracle_bias_grad.argtypes = [_I64, _I64, _D, _D]
     lib.oracle_backward_dw_entries.restype = None
     lib.oracle_backward_dw_entries.argtypes = [
         ctypes.c_int, _I64, _I64, _I64, _I64, _D, _D, _I64,
@@ -156,6 +158,16 @@ def backward_dw(variant, n_in, n_out, D, dZ, X, want_db=True):
     lib.oracle_backward_dw(_variant(variant), n_in, n_out, D, M, _ptr(dZ), _ptr(X),
                            _ptr(dW1), _ptr(dW2), _ptr(db))
     return dW1, dW2, db
+
+
+def bias_grad(dZ):
+    """db = sum over tokens of dZ."""
+    lib = _load()
+    dZ = _f64(dZ)
+    M, n_out = dZ.shape
+    db = np.empty((n_out,), np.float64)
+    lib.oracle_bias_grad(n_out, M, _ptr(dZ), _ptr(db))
+    return db
 
 
 def backward_dw_entries(variant, n_in, n_out, D, dZ, X, comp, i, j, k):

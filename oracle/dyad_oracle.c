@@ -153,6 +153,19 @@ void oracle_backward_dx(int variant, int64_t n_in, int64_t n_out, int64_t D, int
     }
 }
 
+/* Bias gradient: db[f] = sum_m dZ[m][f]. */
+void oracle_bias_grad(int64_t n_out, int64_t M, const double *dZ, double *db)
+{
+    int64_t f;
+#pragma omp parallel for schedule(static)
+    for (f = 0; f < n_out; ++f) {
+        double s = 0.0;
+        for (int64_t m = 0; m < M; ++m)
+            s += dZ[m * n_out + f];
+        db[f] = s;
+    }
+}
+
 /*
  * Weight and bias gradients: dW_c[i][j][k] = sum_m dZ[m][row] X[m][col],
  * db[f] = sum_m dZ[m][f].  db may be NULL.
@@ -176,16 +189,8 @@ void oracle_backward_dw(int variant, int64_t n_in, int64_t n_out, int64_t D, int
             dW[(i * bo + j) * bi + k] = s;
         }
     }
-    if (db) {
-        int64_t f;
-#pragma omp parallel for schedule(static)
-        for (f = 0; f < n_out; ++f) {
-            double s = 0.0;
-            for (int64_t m = 0; m < M; ++m)
-                s += dZ[m * n_out + f];
-            db[f] = s;
-        }
-    }
+    if (db)
+        oracle_bias_grad(n_out, M, dZ, db);
 }
 
 /*

@@ -1,0 +1,127 @@
+// The C-ABI of libdyad (include/dyad.h): argument checks, the choice of kernel
+// for each pass, and launches on the caller's stream.  Every check runs before
+// the first HIP call.
+#include "dyad.h"
+
+#include "dyad_internal.h"
+
+namespace {
+
+using dyad::DwPass;
+using dyad::GemmPass;
+
+constexpr int64_t kMaxDim = (int64_t)1 << 31;   // any single width or token count
+constexpr int64_t kMaxElems = (int64_t)1 << 40; // any single tensor, in elements
+
+bool aligned16(const void *p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
+
+int check_sizes(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t M, int dtype) {
+    if (variant != DYAD_IT && variant != DYAD_OT && variant != DYAD_DT) return DYAD_ERR_INVALID_ARG;
+    if (dtype != DYAD_F32 && dtype != DYAD_BF16) return DYAD_ERR_DTYPE;
+    if (n_in <= 0 || n_out <= 0 || D <= 0 || M < 0) return DYAD_ERR_INVALID_ARG;
+    if (n_in >= kMaxDim || n_out >= kMaxDim || M >= kMaxDim) return DYAD_ERR_INVALID_ARG;
+    if (M * n_in >= kMaxElems || M * n_out >= kMaxElems) return DYAD_ERR_INVALID_ARG;
+    if (n_in % D || n_out % D) return DYAD_ERR_SHAPE;
+    return DYAD_OK;
+}
+
+bool in_transposed(int v) { return v == DYAD_IT || v == DYAD_DT; }
+bool out_transposed(int v) { return v == DYAD_OT || v == DYAD_DT; }
+
+int launch_status(hipError_t e) { return e == hipSuccess ? DYAD_OK : DYAD_ERR_LAUNCH; }
+
+int run_gemm(const GemmPass &p, hipStream_t s) {
+    return launch_status(dyad::launch_simt_gemm(p, s));
+}
+
+size_t dw_workspace(const DwPass &) { return 0; }
+
+}  // namespace
+
+extern "C" {
+
+int dyad_forward(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                 dyad_dtype dtype, const void *X, const void *W1, const void *W2, const void *bias,
+                 dyad_act act, void *Y, void *H, hipStream_t stream) {
+    int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
+    if (rc) return rc;
+    if (act != DYAD_ACT_NONE && act != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
+    if (!W1 || !W2 || (M > 0 && (!X || !Y))) return DYAD_ERR_INVALID_ARG;
+    if (act == DYAD_ACT_NONE) H = nullptr;
+    if (!aligned16(X) || !aligned16(W1) || !aligned16(W2) || !aligned16(bias) || !aligned16(Y) ||
+        !aligned16(H))
+        return DYAD_ERR_ALIGN;
+    if (M == 0) return DYAD_OK;
+    GemmPass p{};
+    p.M = M; p.Kin = n_in; p.Nout = n_out; p.D = n_dyad; p.bk = n_in / n_dyad; p.bn = n_out / n_dyad;
+    p.in_t = in_transposed(variant); p.out_t = out_transposed(variant); p.w_t = false;
+    p.dtype = dtype;
+    p.epilogue = act == DYAD_ACT_GELU ? dyad::kEpiBiasGelu : dyad::kEpiBias;
+    p.in = X; p.W1 = W1; p.W2 = W2; p.bias = bias; p.h_in = nullptr; p.out = Y; p.h_out = H;
+    return run_gemm(p, stream);
+}
+
+int dyad_backward_dx(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype, const void *dZ, const void *W1, const void *W2, dyad_act act_in,
+                     const void *H_in, void *dX, hipStream_t stream) {
+    int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
+    if (rc) return rc;
+    if (act_in != DYAD_ACT_NONE && act_in != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
+    if (!W1 || !W2 || (M > 0 && (!dZ || !dX))) return DYAD_ERR_INVALID_ARG;
+    if (act_in == DYAD_ACT_GELU && M > 0 && !H_in) return DYAD_ERR_INVALID_ARG;
+    if (act_in == DYAD_ACT_NONE) H_in = nullptr;
+    if (!aligned16(dZ) || !aligned16(W1) || !aligned16(W2) || !aligned16(H_in) || !aligned16(dX))
+        return DYAD_ERR_ALIGN;
+    if (M == 0) return DYAD_OK;
+    GemmPass p{};
+    p.M = M; p.Kin = n_out; p.Nout = n_in; p.D = n_dyad; p.bk = n_out / n_dyad; p.bn = n_in / n_dyad;
+    p.in_t = out_transposed(variant); p.out_t = in_transposed(variant); p.w_t = true;
+    p.dtype = dtype;
+    p.epilogue = act_in == DYAD_ACT_GELU ? dyad::kEpiGeluGrad : dyad::kEpiBias;
+    p.in = dZ; p.W1 = W1; p.W2 = W2; p.bias = nullptr; p.h_in = H_in; p.out = dX; p.h_out = nullptr;
+    return run_gemm(p, stream);
+}
+
+static DwPass make_dw(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t M, int dtype) {
+    DwPass p{};
+    p.M = M; p.n_in = n_in; p.n_out = n_out; p.D = D; p.bi = n_in / D; p.bo = n_out / D;
+    p.in_t = in_transposed(variant); p.out_t = out_transposed(variant); p.dtype = dtype;
+    return p;
+}
+
+size_t dyad_dw_workspace_bytes(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad,
+                               int64_t M, dyad_dtype dtype) {
+    if (check_sizes(variant, n_in, n_out, n_dyad, M, dtype)) return 0;
+    return dw_workspace(make_dw(variant, n_in, n_out, n_dyad, M, dtype));
+}
+
+int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype, const void *dZ, const void *X, void *dW1, void *dW2, void *dbias,
+                     void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
+    if (rc) return rc;
+    if (!dW1 || !dW2 || (M > 0 && (!dZ || !X))) return DYAD_ERR_INVALID_ARG;
+    if (!aligned16(dZ) || !aligned16(X) || !aligned16(dW1) || !aligned16(dW2) || !aligned16(dbias) ||
+        !aligned16(workspace))
+        return DYAD_ERR_ALIGN;
+    DwPass p = make_dw(variant, n_in, n_out, n_dyad, M, dtype);
+    size_t need = dw_workspace(p);
+    if (need > 0 && (!workspace || workspace_bytes < need)) return DYAD_ERR_WORKSPACE;
+    p.dZ = dZ; p.X = X; p.dW1 = dW1; p.dW2 = dW2; p.db = dbias; p.ws = workspace; p.ws_bytes = workspace_bytes;
+    return launch_status(dyad::launch_simt_dw(p, stream));
+}
+
+const char *dyad_strerror(int status) {
+    switch (status) {
+    case DYAD_OK: return "ok";
+    case DYAD_ERR_INVALID_ARG: return "invalid argument (enum, size or NULL pointer)";
+    case DYAD_ERR_SHAPE: return "n_in and n_out must be divisible by n_dyad";
+    case DYAD_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case DYAD_ERR_DTYPE: return "unsupported dtype";
+    case DYAD_ERR_WORKSPACE: return "dW workspace missing or too small";
+    case DYAD_ERR_LAUNCH: return "kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// Internal interface between the C-ABI layer (dyad_abi.hip) and the kernel
+// translation units.  Not installed; the public interface is include/dyad.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dyad {
+
+enum Dtype { kF32 = 0, kBF16 = 1 };
+
+// Epilogue applied to the fp32 accumulator of a grouped-GEMM pass.
+enum Epilogue {
+    kEpiBias = 0,      // out = acc + bias (bias may be null)
+    kEpiBiasGelu = 1,  // pre = acc + bias; h_out = pre (if non-null); out = GELU(pre)
+    kEpiGeluGrad = 2,  // out = acc * GELU'(h_in)
+};
+
+// One pass of the Dyad grouped GEMM, written for both the forward pass and the
+// input gradient.  With D groups, per-group input width bk = Kin/D and output
+// width bn = Nout/D, for every token m and output feature f:
+//   out[m][f] = sum over the stored entries (c, i, j, k) whose output column is f
+//               of Wc(i, j, k) * in[m][input column of (c, i, k)]
+// where
+//   output column: comp 1 -> i*bn + j;  comp 2 -> out_t ? j*D + i : i*bn + j
+//   input column:  comp 1 -> i*bk + k;  comp 2 -> in_t  ? k*D + i : i*bk + k
+//   Wc(i, j, k) = w_t ? Wc[i][k][j] (stored [D][bk][bn]) : Wc[i][j][k] (stored [D][bn][bk]).
+// Forward: in = X, out = Y, Kin = n_in, Nout = n_out, in_t = IT|DT, out_t = OT|DT, w_t = 0.
+// Input gradient: in = dZ, out = dX, Kin = n_out, Nout = n_in, in_t = OT|DT,
+// out_t = IT|DT, w_t = 1 (dX = W^T dZ reads every block transposed).
+struct GemmPass {
+    int64_t M, Kin, Nout, D, bk, bn;
+    bool in_t, out_t, w_t;
+    int dtype;       // Dtype
+    int epilogue;    // Epilogue
+    const void *in, *W1, *W2, *bias, *h_in;
+    void *out, *h_out;
+};
+
+// Weight/bias gradient of one layer (forward-variant flags in_t/out_t):
+//   dWc[i][j][k] = sum_m dZ[m][row_c(i, j)] * X[m][col_c(i, k)],  db[f] = sum_m dZ[m][f]
+// row_c = comp 1 or !out_t ? i*bo + j : j*D + i;  col_c = comp 1 or !in_t ? i*bi + k : k*D + i.
+struct DwPass {
+    int64_t M, n_in, n_out, D, bi, bo;
+    bool in_t, out_t;
+    int dtype;
+    const void *dZ, *X;
+    void *dW1, *dW2, *db;
+    void *ws;
+    size_t ws_bytes;
+};
+
+// SIMT kernels: any shape, any D, both dtypes.
+hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t s);
+hipError_t launch_simt_dw(const DwPass &p, hipStream_t s);
+
+}  // namespace dyad

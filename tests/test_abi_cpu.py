@@ -1,0 +1,107 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+declared in include/dyad.h, and rejects bad arguments before any HIP call."""
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2312_06881_amd as dy
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dyad.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dyad_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("dyad_forward", "dyad_backward_dx", "dyad_backward_dw", "dyad_dw_workspace_bytes",
+              "dyad_strerror"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", dy.lib_path()], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s+(\w+)", out))
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    lib = dy._load()
+    for n in declared_functions():
+        assert hasattr(lib, n)
+
+
+def test_binding_exposes_the_same_names():
+    for n in declared_functions():
+        assert callable(getattr(dy, n))
+
+
+def test_strerror():
+    for code in range(-6, 1):
+        assert dy.dyad_strerror(code) and dy.dyad_strerror(code) != "unknown status"
+    assert dy.dyad_strerror(-99) == "unknown status"
+
+
+FAKE = 1 << 20  # a 16-byte-aligned non-NULL address; never dereferenced by rejected calls
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(variant=3), -1),
+    (dict(variant=-1), -1),
+    (dict(dtype=7), -4),
+    (dict(n_in=0), -1),
+    (dict(n_out=-4), -1),
+    (dict(n_dyad=0), -1),
+    (dict(M=-1), -1),
+    (dict(n_in=66), -2),
+    (dict(n_out=258), -2),
+    (dict(M=1 << 31), -1),
+    (dict(W1=None), -1),
+    (dict(X=None), -1),
+    (dict(Y=None), -1),
+    (dict(X=FAKE + 8), -3),
+    (dict(bias=FAKE + 2), -3),
+    (dict(act=5), -1),
+])
+def test_forward_rejects(args, code):
+    a = dict(variant=0, n_in=64, n_out=256, n_dyad=4, M=8, dtype=1, X=FAKE, W1=FAKE, W2=FAKE,
+             bias=None, act=0, Y=FAKE, H=None, stream=None)
+    a.update(args)
+    assert dy.dyad_forward(**a) == code
+
+
+def test_forward_empty_batch_is_a_noop():
+    assert dy.dyad_forward(0, 64, 256, 4, 0, 1, None, FAKE, FAKE, None, 0, None, None, None) == 0
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(act_in=1, H_in=None), -1),
+    (dict(act_in=2), -1),
+    (dict(dZ=None), -1),
+    (dict(dX=FAKE + 4), -3),
+    (dict(n_in=63), -2),
+])
+def test_backward_dx_rejects(args, code):
+    a = dict(variant=1, n_in=64, n_out=256, n_dyad=4, M=8, dtype=1, dZ=FAKE, W1=FAKE, W2=FAKE,
+             act_in=0, H_in=None, dX=FAKE, stream=None)
+    a.update(args)
+    assert dy.dyad_backward_dx(**a) == code
+
+
+def test_backward_dw_rejects_and_workspace_size():
+    a = dict(variant=2, n_in=768, n_out=3072, n_dyad=4, M=16384, dtype=1, dZ=FAKE, X=FAKE,
+             dW1=FAKE, dW2=FAKE, dbias=None, workspace=None, workspace_bytes=0, stream=None)
+    need = dy.dyad_dw_workspace_bytes(2, 768, 3072, 4, 16384, 1)
+    if need:
+        assert dy.dyad_backward_dw(**a) == -5
+        assert dy.dyad_backward_dw(**dict(a, workspace=FAKE, workspace_bytes=need - 1)) == -5
+    assert dy.dyad_backward_dw(**dict(a, dW2=None)) == -1
+    assert dy.dyad_backward_dw(**dict(a, X=FAKE + 1)) == -3
+    assert dy.dyad_backward_dw(**dict(a, n_dyad=5)) == -2
+    assert dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 1) == 0
+    assert dy.dyad_dw_workspace_bytes(9, 768, 3072, 4, 16384, 1) == 0
