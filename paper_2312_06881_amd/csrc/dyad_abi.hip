@@ -31,10 +31,12 @@ bool out_transposed(int v) { return v == DYAD_OT || v == DYAD_DT; }
 int launch_status(hipError_t e) { return e == hipSuccess ? DYAD_OK : DYAD_ERR_LAUNCH; }
 
 int run_gemm(const GemmPass &p, hipStream_t s) {
-    return launch_status(dyad::launch_simt_gemm(p, s));
+    hipError_t e = dyad::launch_mfma_gemm(p, s);
+    if (e == hipErrorNotSupported) e = dyad::launch_simt_gemm(p, s);
+    return launch_status(e);
 }
 
-size_t dw_workspace(const DwPass &) { return 0; }
+size_t dw_workspace(const DwPass &p) { return dyad::mfma_dw_workspace(p); }
 
 }  // namespace
 
@@ -108,7 +110,9 @@ int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t 
     size_t need = dw_workspace(p);
     if (need > 0 && (!workspace || workspace_bytes < need)) return DYAD_ERR_WORKSPACE;
     p.dZ = dZ; p.X = X; p.dW1 = dW1; p.dW2 = dW2; p.db = dbias; p.ws = workspace; p.ws_bytes = workspace_bytes;
-    return launch_status(dyad::launch_simt_dw(p, stream));
+    hipError_t e = need > 0 ? dyad::launch_mfma_dw(p, stream) : hipErrorNotSupported;
+    if (e == hipErrorNotSupported) e = dyad::launch_simt_dw(p, stream);
+    return launch_status(e);
 }
 
 const char *dyad_strerror(int status) {

@@ -54,4 +54,14 @@ struct DwPass {
 hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t s);
 hipError_t launch_simt_dw(const DwPass &p, hipStream_t s);
 
+// MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
+// when the pass's shape has no matching tile configuration.
+hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t s);
+
+// MFMA weight gradient (bf16): split over tokens, fixed-order reduction of the
+// splits through the workspace.  mfma_dw_workspace() is 0 when the shape is not
+// covered, and launch_mfma_dw() then returns hipErrorNotSupported.
+size_t mfma_dw_workspace(const DwPass &p);
+hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s);
+
 }  // namespace dyad

@@ -28,6 +28,8 @@ SMALL = [  # (n_in, n_out, n_dyad, M)
     (512, 2048, 16, 77),
     (256, 256, 2, 100),
     (256, 256, 1, 100),
+    (1024, 1024, 8, 129),
+    (4096, 4096, 16, 70),
     (192, 96, 3, 50),     # odd n_dyad, block widths 64 and 32
     (40, 24, 8, 33),      # block widths 5 and 3
 ]
@@ -258,3 +260,19 @@ def test_full_size_ff_sampled(wl, variant):
         banner("full", wl.name, name, variant)
         check_full_layer(n_in, n_out, wl.n_dyad, wl.M, variant, "gelu" if name == "fc2" else "none",
                          seed_offset=li)
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", [(768, 3072, 4, 5000), (3072, 768, 4, 3001), (1024, 1024, 16, 2049)],
+                         ids=case_id)
+def test_backward_dw_many_splits(shape, variant):
+    """Token counts that spread over many splits, with a ragged last split."""
+    n_in, n_out, D, M = shape
+    banner("backward_dw_splits", shape, variant)
+    L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=3)
+    dw1, dw2, db = dy.backward_dw(gpu(L.dZ), gpu(L.X), D, variant=variant)
+    torch.cuda.synchronize()
+    r1, r2, rb = oracle.backward_dw(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"))
+    assert_close(dw1, r1, "bf16", "dW1")
+    assert_close(dw2, r2, "bf16", "dW2")
+    assert_close(db, rb, "bf16", "db")
