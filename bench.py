@@ -1,19 +1,19 @@
-"""Benchmark: Dyad feed-forward fwd+bwd on one MI355X.
+"""Benchmark: the Dyad feed-forward block, forward and backward, on one MI355X.
 
-One step = for each of Dyad-IT, -OT, -DT, the feed-forward block of the chosen
-workload (default: OPT-125m shapes, fc1 768->3072 with GELU, fc2 3072->768,
-n_dyad=4, M=16384 tokens, bf16 with fp32 accumulation) run forward and
-backward through libdyad: fc1 fwd (GELU, pre-activation stashed), fc2 fwd,
-fc2 dX (GELU' fused), fc2 dW+db, fc1 dX, fc1 dW+db.  FLOPs are counted
+One step = for each of Dyad-IT, -OT and -DT, the feed-forward block of the
+chosen workload (default: OPT-125m shapes, fc1 768->3072 with GELU, fc2
+3072->768, n_dyad=4, M=16384 tokens, bf16 with fp32 accumulation) run forward
+and backward through libdyad's C-ABI: fc1 forward (GELU, pre-activation
+stashed), fc2 forward, fc2 input gradient (GELU' fused), fc2 weight+bias
+gradient, fc1 input gradient, fc1 weight+bias gradient.  FLOPs are counted
 algorithmically, 4*M*n_in*n_out/n_dyad per pass.
 
-Prints one JSON line.  Inputs are seeded synthetic tensors already resident
-in HBM when the timed region starts.
+Prints one JSON line.  Inputs are seeded synthetic tensors already resident in
+HBM when the timed region starts.
 """
 from __future__ import annotations
 
 import argparse
-import ctypes
 import hashlib
 import json
 import os
@@ -24,7 +24,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
-PEAK_HBM_GBS = 8000.0
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # FLOP per byte
+METRIC = "Dyad fwd+bwd TFLOP/s and % bf16 MFMA peak; speedup vs dense GEMM, same shape"
 
 
 def parse():
@@ -36,7 +38,9 @@ def parse():
     ap.add_argument("--variants", default="IT,OT,DT")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=2048)
+    ap.add_argument("--cpu-tokens", type=int, default=16384)
+    ap.add_argument("--only", default="",
+                    help="run just this call (e.g. IT:fc1.fwd) --steps times, for counter collection")
     return ap.parse_args()
 
 
@@ -48,28 +52,74 @@ def workload(name):
     return table[name]
 
 
+def algorithmic_bytes(kind, n_in, n_out, D, M, e=2, gelu=False, stash=False):
+    """Bytes one pass must move: its operands and results, each once."""
+    w = 2 * n_in * n_out // D
+    if kind == "fwd":
+        return e * (M * n_in + M * n_out + w + n_out + (M * n_out if stash else 0))
+    if kind == "dx":
+        return e * (M * n_out + w + M * n_in + (M * n_in if gelu else 0))
+    return e * (M * n_out + M * n_in + w + n_out)
+
+
 class Layer:
     """Device buffers of one Dyad layer, allocated once."""
 
-    def __init__(self, dy, torch, n_in, n_out, D, M, act, seed_offset, dev):
+    def __init__(self, torch, n_in, n_out, D, M, seed_offset, dev):
         from workloads import layer_inputs
         L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=seed_offset)
-        self.n_in, self.n_out, self.D, self.M, self.act = n_in, n_out, D, M, act
+        self.n_in, self.n_out, self.D, self.M = n_in, n_out, D, M
         self.W1, self.W2, self.b = L.W1.to(dev), L.W2.to(dev), L.bias.to(dev)
         self.dW1, self.dW2 = torch.empty_like(self.W1), torch.empty_like(self.W2)
         self.db = torch.empty_like(self.b)
         self.X0 = L.X.to(dev)      # input of the first layer
         self.dZ0 = L.dZ.to(dev)    # upstream gradient of the last layer
         self.Y = torch.empty((M, n_out), dtype=torch.bfloat16, device=dev)
-        self.H = torch.empty_like(self.Y) if act else None
+        self.H = torch.empty_like(self.Y)
         self.dX = torch.empty((M, n_in), dtype=torch.bfloat16, device=dev)
         self.flops = 4.0 * M * n_in * n_out / D
+
+
+def build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp):
+    """(name, flops, bytes, fn) for every C-ABI call of one step, in step order."""
+    D, M = wl.n_dyad, wl.M
+    vid = {"IT": dy.IT, "OT": dy.OT, "DT": dy.DT}
+
+    def p(t):
+        return None if t is None else t.data_ptr()
+
+    out = []
+    for v in variants:
+        V = vid[v]
+        ab = lambda kind, L, **kw: algorithmic_bytes(kind, L.n_in, L.n_out, D, M, **kw)  # noqa: E731
+        out += [
+            (f"{v}:fc1.fwd", fc1.flops, ab("fwd", fc1, stash=True),
+             lambda V=V: lib.dyad_forward(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc1.X0), p(fc1.W1),
+                                          p(fc1.W2), p(fc1.b), dy.ACT_GELU, p(fc1.Y), p(fc1.H), sp)),
+            (f"{v}:fc2.fwd", fc2.flops, ab("fwd", fc2),
+             lambda V=V: lib.dyad_forward(V, fc2.n_in, fc2.n_out, D, M, dy.BF16, p(fc1.Y), p(fc2.W1),
+                                          p(fc2.W2), p(fc2.b), dy.ACT_NONE, p(fc2.Y), None, sp)),
+            (f"{v}:fc2.dx", fc2.flops, ab("dx", fc2, gelu=True),
+             lambda V=V: lib.dyad_backward_dx(V, fc2.n_in, fc2.n_out, D, M, dy.BF16, p(fc2.dZ0),
+                                              p(fc2.W1), p(fc2.W2), dy.ACT_GELU, p(fc1.H), p(fc2.dX), sp)),
+            (f"{v}:fc2.dw", fc2.flops, ab("dw", fc2),
+             lambda V=V: lib.dyad_backward_dw(V, fc2.n_in, fc2.n_out, D, M, dy.BF16, p(fc2.dZ0), p(fc1.Y),
+                                              p(fc2.dW1), p(fc2.dW2), p(fc2.db), p(ws), ws_bytes, sp)),
+            (f"{v}:fc1.dx", fc1.flops, ab("dx", fc1),
+             lambda V=V: lib.dyad_backward_dx(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc2.dX), p(fc1.W1),
+                                              p(fc1.W2), dy.ACT_NONE, None, p(fc1.dX), sp)),
+            (f"{v}:fc1.dw", fc1.flops, ab("dw", fc1),
+             lambda V=V: lib.dyad_backward_dw(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc2.dX), p(fc1.X0),
+                                              p(fc1.dW1), p(fc1.dW2), p(fc1.db), p(ws), ws_bytes, sp)),
+        ]
+    return out
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(the multi-GPU design is described, not built)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
@@ -85,56 +135,48 @@ def main():
     variants = [v for v in args.variants.split(",") if v]
     vid = {"IT": dy.IT, "OT": dy.OT, "DT": dy.DT}
 
-    (n1, i1, o1), (n2, i2, o2) = wl.layers if len(wl.layers) == 2 else (wl.layers[0], wl.layers[0])
-    fc1 = Layer(dy, torch, i1, o1, D, M, True, 0, dev)
-    fc2 = Layer(dy, torch, i2, o2, D, M, False, 1, dev)
+    if len(wl.layers) == 2:
+        (_, i1, o1), (_, i2, o2) = wl.layers
+    else:
+        (_, i1, o1), = wl.layers
+        i2, o2 = o1, i1
+    fc1 = Layer(torch, i1, o1, D, M, 0, dev)
+    fc2 = Layer(torch, i2, o2, D, M, 1, dev)
     ws_bytes = max(dy.dyad_dw_workspace_bytes(vid[v], L.n_in, L.n_out, D, M, dy.BF16)
                    for v in variants for L in (fc1, fc2))
     ws = torch.empty((max(ws_bytes, 16),), dtype=torch.uint8, device=dev)
-
-    def p(t):
-        return None if t is None else t.data_ptr()
 
     def check(rc):
         if rc != 0:
             raise RuntimeError(dy.dyad_strerror(rc))
 
-    # one call = one entry point of the C-ABI; kind: "gemm" (fwd / dX) or "dw"
-    def calls(v):
-        V = vid[v]
-        return [
-            ("gemm", fc1.flops, lambda: lib.dyad_forward(V, fc1.n_in, fc1.n_out, D, M, dy.BF16,
-                                                        p(fc1.X0), p(fc1.W1), p(fc1.W2), p(fc1.b),
-                                                        dy.ACT_GELU, p(fc1.Y), p(fc1.H), sp)),
-            ("gemm", fc2.flops, lambda: lib.dyad_forward(V, fc2.n_in, fc2.n_out, D, M, dy.BF16,
-                                                        p(fc1.Y), p(fc2.W1), p(fc2.W2), p(fc2.b),
-                                                        dy.ACT_NONE, p(fc2.Y), None, sp)),
-            ("gemm", fc2.flops, lambda: lib.dyad_backward_dx(V, fc2.n_in, fc2.n_out, D, M, dy.BF16,
-                                                            p(fc2.dZ0), p(fc2.W1), p(fc2.W2),
-                                                            dy.ACT_GELU, p(fc1.H), p(fc2.dX), sp)),
-            ("dw", fc2.flops, lambda: lib.dyad_backward_dw(V, fc2.n_in, fc2.n_out, D, M, dy.BF16,
-                                                          p(fc2.dZ0), p(fc1.Y), p(fc2.dW1),
-                                                          p(fc2.dW2), p(fc2.db), p(ws), ws_bytes, sp)),
-            ("gemm", fc1.flops, lambda: lib.dyad_backward_dx(V, fc1.n_in, fc1.n_out, D, M, dy.BF16,
-                                                            p(fc2.dX), p(fc1.W1), p(fc1.W2),
-                                                            dy.ACT_NONE, None, p(fc1.dX), sp)),
-            ("dw", fc1.flops, lambda: lib.dyad_backward_dw(V, fc1.n_in, fc1.n_out, D, M, dy.BF16,
-                                                          p(fc2.dX), p(fc1.X0), p(fc1.dW1),
-                                                          p(fc1.dW2), p(fc1.db), p(ws), ws_bytes, sp)),
-        ]
+    calls = build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp)
+    if args.only:
+        # counter collection: one call, repeated, plus a plain copy of known size
+        sel = [c for c in calls if c[0] == args.only]
+        if not sel:
+            raise SystemExit(f"--only {args.only}: no such call; one of {[c[0] for c in calls]}")
+        src = torch.empty((256 << 20,), dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            check(sel[0][3]())
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": args.only, "launches": args.steps, "copy_bytes": src.numel(),
+                          "algorithmic_bytes": sel[0][2], "flops": sel[0][1]}))
+        return
 
-    step_calls = [(v, c) for v in variants for c in calls(v)]
-    flops_step = sum(c[1] for _, c in step_calls)
+    flops_step = sum(c[1] for c in calls)
 
     def step():
-        for _, (_, _, fn) in step_calls:
-            check(fn())
+        for c in calls:
+            check(c[3]())
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # timed region: K steps, events on the launch stream only at its ends
+    # timed region: K whole steps between two events on the launch stream
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -148,72 +190,50 @@ def main():
     ms_step = t0.elapsed_time(t1) / args.steps
     tflops = flops_step / (ms_step * 1e-3) / 1e12
 
-    # per-launch durations: the same K steps again, an event pair around every call
-    per = {}
+    # per-call durations: K more steps with an event pair around every call
     evs = []
     for _ in range(args.steps):
-        for v, (kind, fl, fn) in step_calls:
+        for c in calls:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            check(fn())
+            check(c[3]())
             b.record(stream)
-            evs.append((v, kind, fl, a, b))
+            evs.append((c, a, b))
     torch.cuda.synchronize()
-    for v, kind, fl, a, b in evs:
-        d = per.setdefault(kind, {"ms": 0.0, "n": 0, "flops": 0.0})
+    per = {}
+    for c, a, b in evs:
+        d = per.setdefault(c[0], {"ms": 0.0, "n": 0, "flops": c[1], "bytes": c[2]})
         d["ms"] += a.elapsed_time(b)
         d["n"] += 1
-        d["flops"] += fl
-        dv = per.setdefault(f"{v}", {"ms": 0.0, "n": 0, "flops": 0.0})
-        dv["ms"] += a.elapsed_time(b)
-        dv["n"] += 1
-        dv["flops"] += fl
-    dom = max(("gemm", "dw"), key=lambda k: per[k]["ms"])
-    avg_ms = per[dom]["ms"] / per[dom]["n"]
-    fl_launch = per[dom]["flops"] / per[dom]["n"]
-    achieved = fl_launch / (avg_ms * 1e-3) / 1e12
-    per_variant = {v: round(per[v]["flops"] / (per[v]["ms"] * 1e-3) / 1e12, 1) for v in variants}
+    table = {}
+    for name, d in per.items():
+        us = d["ms"] / d["n"] * 1e3
+        table[name] = {"us": round(us, 2), "tflops": round(d["flops"] / (us * 1e-6) / 1e12, 1),
+                       "gbs": round(d["bytes"] / (us * 1e-6) / 1e9, 1),
+                       "bound": "hbm" if d["flops"] / d["bytes"] < RIDGE else "mfma"}
+    dom = max(per, key=lambda n: per[n]["ms"])
+    dd = per[dom]
+    avg_s = dd["ms"] / dd["n"] * 1e-3
+    if table[dom]["bound"] == "hbm":
+        achieved, peak, unit = dd["bytes"] / avg_s / 1e9, PEAK_HBM_GBS, "GB/s"
+    else:
+        achieved, peak, unit = dd["flops"] / avg_s / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+    per_variant = {}
+    for v in variants:
+        ms_v = sum(per[n]["ms"] / per[n]["n"] for n in per if n.startswith(v + ":"))
+        fl_v = sum(per[n]["flops"] for n in per if n.startswith(v + ":"))
+        per_variant[v] = {"ms": round(ms_v, 4), "tflops": round(fl_v / (ms_v * 1e-3) / 1e12, 1)}
 
-    # dense baseline: same shapes through torch (hipBLASLt), fwd + dX + dW per layer
     dense = None
     if not args.no_dense:
-        xs = {}
-        for L in (fc1, fc2):
-            xs[L] = (torch.randn((L.n_out, L.n_in), device=dev).mul_(0.02).to(torch.bfloat16),
-                     torch.randn((M, L.n_in), device=dev).to(torch.bfloat16),
-                     torch.randn((M, L.n_out), device=dev).to(torch.bfloat16))
+        dense = dense_baseline(torch, fc1, fc2, M, dev, stream, args)
+        dense["speedup"] = {v: round(dense["ms_per_ff_fwd_bwd"] / per_variant[v]["ms"], 3)
+                            for v in variants}
 
-        def dense_ff():
-            for L in (fc1, fc2):
-                Wd, Xd, dZd = xs[L]
-                torch.addmm(L.b, Xd, Wd.t())
-                torch.mm(dZd, Wd)
-                torch.mm(dZd.t(), Xd)
-                dZd.sum(0)
-        for _ in range(args.warmup):
-            dense_ff()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            dense_ff()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        dense_ms = e0.elapsed_time(e1) / args.steps
-        dyad_ms_per_variant = {v: per[v]["ms"] / args.steps for v in variants}
-        dense_flops = sum(3 * 2.0 * M * L.n_in * L.n_out for L in (fc1, fc2))
-        dense = {"ms_per_ff_fwd_bwd": round(dense_ms, 4),
-                 "tflops": round(dense_flops / (dense_ms * 1e-3) / 1e12, 1),
-                 "speedup": {v: round(dense_ms / dyad_ms_per_variant[v], 3) for v in variants}}
+    cpu = None if args.no_cpu else cpu_baseline(wl, args.cpu_tokens)
 
-    # CPU oracle on a bounded token sample (reported baseline only)
-    cpu = None
-    if not args.no_cpu:
-        cpu = cpu_baseline(wl, args.cpu_tokens)
-
-    traffic = read_traffic(dom, args.workload)
     out = {
-        "metric": "Dyad fwd+bwd TFLOP/s and % bf16 MFMA peak; speedup vs dense GEMM, same shape",
+        "metric": METRIC,
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -227,25 +247,58 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.note, "n_dyad": D, "tokens": M,
                    "layers": [list(l) for l in wl.layers], "variants": variants,
-                   "step": "per variant: fc1 fwd(GELU)+fc2 fwd+fc2 dX(GELU')+fc2 dW+fc1 dX+fc1 dW"},
+                   "step": "per variant: fc1 fwd(GELU, stash) + fc2 fwd + fc2 dX(GELU') + fc2 dW+db "
+                           "+ fc1 dX + fc1 dW+db"},
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
-        "tflops_per_variant": per_variant,
+        "per_variant": per_variant,
         "speedup_vs_dense": dense["speedup"] if dense else None,
         "dense": dense,
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "avg_launch_us": round(avg_ms * 1e3, 2),
-                     "flops_per_launch": fl_launch, "traffic": traffic},
+        "roofline": {"bound": table[dom]["bound"], "call": dom, "achieved": round(achieved, 1),
+                     "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
+                     "avg_launch_us": round(avg_s * 1e6, 2), "flops_per_launch": dd["flops"],
+                     "bytes_per_launch": dd["bytes"],
+                     "traffic": read_traffic(dom, wl.name)},
+        "per_call": table,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
     }
     print(json.dumps(out))
 
 
+def dense_baseline(torch, fc1, fc2, M, dev, stream, args):
+    """Same-shape dense layers through torch (hipBLASLt): fwd X W^T + b, dX = dZ W, dW = dZ^T X, db."""
+    xs = {}
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    for L in (fc1, fc2):
+        xs[L] = (torch.randn((L.n_out, L.n_in), device=dev, generator=g).mul_(0.02).to(torch.bfloat16),
+                 torch.randn((M, L.n_in), device=dev, generator=g).to(torch.bfloat16),
+                 torch.randn((M, L.n_out), device=dev, generator=g).to(torch.bfloat16))
+
+    def dense_ff():
+        for L in (fc1, fc2):
+            Wd, Xd, dZd = xs[L]
+            torch.addmm(L.b, Xd, Wd.t())
+            torch.mm(dZd, Wd)
+            torch.mm(dZd.t(), Xd)
+            dZd.sum(0)
+
+    for _ in range(args.warmup):
+        dense_ff()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        dense_ff()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    flops = sum(3 * 2.0 * M * L.n_in * L.n_out for L in (fc1, fc2))
+    return {"ms_per_ff_fwd_bwd": round(ms, 4), "tflops": round(flops / (ms * 1e-3) / 1e12, 1)}
+
+
 def cpu_baseline(wl, tokens):
-    """The oracle, as is, on the first `tokens` tokens of the same workload (Dyad-IT)."""
-    import numpy as np  # noqa: F401
+    """The oracle, as it stands, on the first `tokens` tokens of the same workload (Dyad-IT)."""
     import oracle
     from workloads import layer_inputs
     D = wl.n_dyad
@@ -262,8 +315,8 @@ def cpu_baseline(wl, tokens):
     dt = time.perf_counter() - t0
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle", "seconds": round(dt, 2),
-            "sample": f"{wl.name}, Dyad-IT, every layer fwd+dX+dW+db on {Ms} of {wl.M} tokens "
-                      f"(fp64 plain loops, OpenMP)"}
+            "sample": f"{wl.name}, Dyad-IT only, every layer fwd + dX + dW + db on {Ms} of {wl.M} "
+                      f"tokens (fp64 plain loops, OpenMP); input generation included"}
 
 
 def kernel_source_hash():
@@ -275,9 +328,9 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel, wl_name):
-    """HBM bytes per launch from a committed rocprofv3 --pmc summary, if it matches these sources."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{wl_name}.json")
+def read_traffic(call, wl_name):
+    """HBM bytes per launch of `call` from a committed counter summary, if it matches these sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{wl_name}.json")
     if not os.path.exists(path):
         return None
     try:
@@ -286,7 +339,7 @@ def read_traffic(kernel, wl_name):
         return None
     if rec.get("source_hash") != kernel_source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("calls", {}).get(call, {}).get("hbm_bytes_per_launch")
 
 
 if __name__ == "__main__":

@@ -5,10 +5,22 @@
 
 namespace dyad {
 
-template <int BM, int BN, int WM, int WN, int D, bool IN_T, bool OUT_T, bool W_T>
+// Workgroups per CU: two when both the tile's LDS and its registers fit twice
+// (two caps a wave at 256 VGPRs, so accumulators above 128 per lane need one).
+template <class C>
+constexpr int occupancy() {
+    const int acc_per_lane = C::WM * C::WN / 64;
+    return ((160 * 1024) / C::kLds >= 2 && acc_per_lane <= 128) ? 2 : 1;
+}
+
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
+    using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
     GemmArgs a;
-    a.M = p.M; a.Kin = p.Kin; a.Nout = p.Nout; a.bk = p.bk; a.bn = p.bn;
+    // buffer offsets are 32-bit: one token panel of the input and one weight tensor must fit
+    if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || 2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
+        return hipErrorNotSupported;
+    a.M = p.M; a.Kin = p.Kin; a.Nout = p.Nout; a.bk = p.bk; a.bn = p.bn; a.D = p.D;
     a.in = static_cast<const uint16_t *>(p.in);
     a.W1 = static_cast<const uint16_t *>(p.W1);
     a.W2 = static_cast<const uint16_t *>(p.W2);
@@ -22,27 +34,27 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     a.tiles_n = (int)tiles_n;
     a.tiles_total = (int)(tiles_m * tiles_n);
-    dyad_gemm_mfma<BM, BN, WM, WN, D, IN_T, OUT_T, W_T><<<a.tiles_total, kThreads, 0, s>>>(a);
+    dyad_gemm_mfma<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, occupancy<C>()>
+        <<<a.tiles_total, C::kThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 
-// Picks the widest tile whose columns stay inside one output block and, with
-// an output transpose, give every residue a multiple of 16 columns.
+// Widest column tile that stays inside one output block; with an output
+// transpose every residue must get a multiple of 16 columns.  A BlockTrans
+// stage with an output transpose stages one A slab per residue, so the token
+// tile shrinks as n_dyad grows to keep both stage buffers in LDS.
 template <int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     if (p.bk % kStageK != 0) return hipErrorNotSupported;
-    if constexpr (D <= 8) {
-        if constexpr (!OUT_T || (128 / D) % 16 == 0)
-            if (p.bn % 128 == 0) return launch_tile<128, 128, 64, 64, D, IN_T, OUT_T, W_T>(p, s);
-        if constexpr (!OUT_T || (192 / D) % 16 == 0)
-            if (p.bn % 192 == 0) return launch_tile<128, 192, 64, 96, D, IN_T, OUT_T, W_T>(p, s);
-        if constexpr (!OUT_T || (64 / D) % 16 == 0)
-            if (p.bn % 64 == 0) return launch_tile<128, 64, 64, 32, D, IN_T, OUT_T, W_T>(p, s);
-    } else {
-        if (p.bn % 256 == 0) return launch_tile<64, 256, 64, 64, D, IN_T, OUT_T, W_T>(p, s);
-        if constexpr (!OUT_T)
-            if (p.bn % 128 == 0) return launch_tile<64, 128, 32, 64, D, IN_T, OUT_T, W_T>(p, s);
-    }
+    constexpr int BM = D >= 8 ? 64 : 128;
+    if constexpr (!OUT_T || (256 / D >= 16 && D < 16))
+        if (p.bn % 256 == 0) return launch_tile<BM, 256, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
+    if constexpr (!OUT_T || (192 % D == 0 && (192 / D) % 16 == 0))
+        if (p.bn % 192 == 0) return launch_tile<BM, 192, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
+    if constexpr (!OUT_T || 128 / D >= 16)
+        if (p.bn % 128 == 0) return launch_tile<BM, 128, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
+    if constexpr (!OUT_T || 64 / D >= 16)
+        if (p.bn % 64 == 0) return launch_tile<BM, 64, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
     return hipErrorNotSupported;
 }
 
