@@ -1,37 +1,38 @@
 // Weight and bias gradients of a Dyad layer on gfx950 matrix cores.
 //
 // dW_c[g][j][k] = sum_m dZ[m][row_c(g, j)] * X[m][col_c(g, k)] is, for each
-// component c and group g, a GEMM whose reduction runs over the tokens.
+// component c and group g, a GEMM whose reduction runs over the M tokens:
+// A = dZ^T restricted to the group's rows, B = X^T restricted to its columns.
 //
-// Work split.  A workgroup owns one component c, a range of J weight rows and
-// K weight columns, for ALL D groups at once, and one contiguous range of
-// tokens (a "split").  Taking every group together means a strided operand --
-// dZ columns j*D + g of an output transpose, X columns k*D + g of an input
-// transpose -- is read as the contiguous span of D*J (or D*K) columns, every
-// element of which belongs to one of the groups: nothing loaded is discarded.
-// The unstrided side reads D block slices.  Each split writes fp32 partial sums
-// to the workspace; a second kernel adds the splits in a fixed order, so the
+// Work split.  A workgroup owns one (component, group) pair, a BJ x BK tile of
+// that group's weight block and one contiguous range of tokens (a "split").
+// Splits are dealt so that every workgroup of one split runs on the same XCD:
+// the split's slice of dZ and X is then fetched from HBM once and served to
+// all of them from that XCD's L2.  Each workgroup writes fp32 partial sums to
+// the workspace; a second kernel adds the splits in a fixed order, so the
 // result is bitwise reproducible.
 //
-// Staging.  Both operands are token-major in memory while the MFMA wants 8
-// consecutive tokens per lane, so each thread loads an 8-token x 8-column
-// block (eight 16-byte loads), transposes it in registers and writes eight
-// 16-byte column vectors into LDS tiles laid out [group][row][token].
+// Pipeline.  Stages of 32 tokens, double-buffered in LDS with the next stage's
+// loads in flight, exactly as in the grouped GEMM, so the MFMA consumes 16x32
+// fragments from 64-byte swizzled LDS rows (row = weight row j or column k,
+// 32 tokens per row).  Both operands are token-major in memory, so each thread
+// loads 8x8 blocks (8 tokens x 8 consecutive columns, eight 16-byte loads) and
+// transposes them in registers (v_perm_b32) on the way into LDS.
 //
-// Bias gradient.  Workgroups of component 1 with K offset 0 also sum their dZ
-// columns over the split's tokens (db partials); every dZ column is covered by
-// exactly one such workgroup.
-#include "dyad_device.h"
+// Strided operands.  The BlockTrans component reads dZ columns j*D + g (output
+// transpose) or X columns k*D + g (input transpose).  Such a side loads the
+// 16-byte vectors that contain its columns -- 8/D consecutive j (or k) per
+// vector for D <= 8 -- and keeps the group's residue only.
+//
+// Bias gradient.  Workgroups of component 1 whose column tile is the first sum
+// their dZ rows over the split's tokens straight from LDS; every dZ column is
+// covered by exactly one such workgroup.
 #include "dyad_internal.h"
+#include "mfma_common.h"
 
 namespace dyad {
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
-
-constexpr int kT = 32;               // tokens per stage (one MFMA K step)
-constexpr int kRowT = kT + 8;        // LDS row pitch in bf16 (padding)
 constexpr int kThreads = 256;
 
 struct DwArgs {
@@ -40,226 +41,247 @@ struct DwArgs {
     float *part;          // [splits][2][D][bo][bi]
     float *part_db;       // [splits][n_out]
     int64_t tokens_per_split;
-    int tiles_j, tiles_k; // per component
-    int splits;
+    int tiles_j, tiles_k; // tiles per (component, group)
+    int splits, splits_per_xcd;
     int want_db;
 };
 
-__device__ __forceinline__ uint4 ldg16(const uint16_t *p) { return *reinterpret_cast<const uint4 *>(p); }
-
-__device__ __forceinline__ uint32_t word(const uint4 &v, int q) {
-    return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
-}
-
-// Column e (0..7) of an 8x8 bf16 block given as 8 rows of 8: the 8 row values, packed.
-__device__ __forceinline__ uint4 column_of(const uint4 (&r)[8], int e) {
-    uint32_t o[4];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const uint32_t a = word(r[2 * p], e >> 1), b = word(r[2 * p + 1], e >> 1);
-        o[p] = (e & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+// Column e (0..7, uniform across the workgroup) of an 8x8 bf16 block: one
+// branch per value, each a compile-time shuffle.
+template <int E = 0>
+__device__ __forceinline__ uint4 column_uniform(const uint4 (&r)[8], int e) {
+    if constexpr (E < 7) {
+        if (e != E) return column_uniform<E + 1>(r, e);
     }
-    return make_uint4(o[0], o[1], o[2], o[3]);
+    return column_of(r, E);
 }
 
-// D groups; per group a J x K output tile; WJ x WK per wave; GPW groups per wave.
-template <int D, int J, int K, int WJ, int WK, bool IN_T, bool OUT_T>
-struct DwTile {
-    static constexpr int kGPW = D >= 4 ? D / 4 : 1;              // groups per wave
-    static constexpr int kWPG = D >= 4 ? 1 : 4 / D;              // waves per group
-    static constexpr int kWavesK = K / WK;                       // within a group
+// One side (A = dZ, B = X) of a workgroup's stage: which source columns it
+// loads and where they land in LDS.  `rows` LDS rows (weight rows j or
+// columns k of the tile), 32 tokens each.
+//   plain:  source column first + row, for row in [0, rows)
+//   strided (SPAN): source column (first + row) * D + g
+template <int D, bool SPAN, int ROWS>
+struct Side {
+    // k values (LDS rows) per loaded 16-byte vector, and vectors per 8 tokens
+    static constexpr int kPerVec = SPAN ? (D <= 8 ? 8 / D : 1) : 8;
+    static constexpr int kVecCols = ROWS / kPerVec;              // vector columns per token row
+    static constexpr int kBlocks = kVecCols * (kStageK / 8);     // 8x8 blocks per stage
+    static_assert(ROWS % kPerVec == 0, "whole vectors per tile");
+};
+
+template <int D, int BJ, int BK, bool IN_T, bool OUT_T>
+struct DwCfg {
+    static constexpr int kWavesJ = 2, kWavesK = 2;
+    static constexpr int WJ = BJ / kWavesJ, WK = BK / kWavesK;
     static constexpr int kSubJ = WJ / 16, kSubK = WK / 16;
-    static constexpr int kRowsA = D * J, kRowsB = D * K;         // LDS rows
-    static constexpr int kBlocksA = kRowsA / 8 * (kT / 8);       // 8x8 blocks per stage
-    static constexpr int kBlocksB = kRowsB / 8 * (kT / 8);
-    static constexpr int kBlocks = kBlocksA + kBlocksB;
-    static constexpr int kIters = (kBlocks + kThreads - 1) / kThreads;
-    static constexpr int kLds = (kRowsA + kRowsB) * kRowT * 2;
-    static_assert(D >= 4 || (J / WJ) * (K / WK) == kWPG, "waves of one group tile it exactly");
-    static_assert(D < 4 || (WJ == J && WK == K), "one wave holds whole group tiles");
+    static constexpr int kStageElems = (BJ + BK) * kStageK;       // bf16 per LDS stage buffer
+    static constexpr int kLds = 2 * kStageElems * 2;
+    static constexpr int kMaxBlocks = 2 * (BJ * D + BK * D) / 8 * (kStageK / 8);
+    static_assert(WJ % 16 == 0 && WK % 16 == 0, "whole MFMA blocks per wave");
     static_assert(kLds <= 160 * 1024, "LDS budget");
 };
 
-template <int D, int J, int K, int WJ, int WK, bool IN_T, bool OUT_T>
-__global__ void __launch_bounds__(kThreads, 1) dyad_dw_mfma(DwArgs a) {
-    using T = DwTile<D, J, K, WJ, WK, IN_T, OUT_T>;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[(T::kRowsA + T::kRowsB) * kRowT];
-    uint16_t *ldsA = lds;                       // [D*J][kRowT]  dZ^T, row = g*J + j
-    uint16_t *ldsB = lds + T::kRowsA * kRowT;   // [D*K][kRowT]  X^T,  row = g*K + k
+template <int D, int BJ, int BK, bool IN_T, bool OUT_T, bool C2>
+__device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, int split, int g, int jt, int kt) {
+    using C = DwCfg<D, BJ, BK, IN_T, OUT_T>;
+    constexpr bool SPAN_A = C2 && OUT_T;    // dZ columns j*D + g
+    constexpr bool SPAN_B = C2 && IN_T;     // X columns k*D + g
+    using SA = Side<D, SPAN_A, BJ>;
+    using SB = Side<D, SPAN_B, BK>;
+    constexpr int kBlkA = SA::kBlocks, kBlk = SA::kBlocks + SB::kBlocks;
+    constexpr int kIters = (kBlk + kThreads - 1) / kThreads;
 
+    uint16_t *lds = reinterpret_cast<uint16_t *>(smem);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // block -> (split, component, j tile, k tile); splits of one tile are adjacent
-    int b = blockIdx.x;
-    const int split = b % a.splits; b /= a.splits;
-    const int kt = b % a.tiles_k; b /= a.tiles_k;
-    const int jt = b % a.tiles_j; b /= a.tiles_j;
-    const int comp = b + 1;
-    const int64_t j0 = (int64_t)jt * J, k0 = (int64_t)kt * K;
+    const int j0 = jt * BJ, k0 = kt * BK;
+    const int bo = (int)a.bo, bi = (int)a.bi, n_out = (int)a.n_out, n_in = (int)a.n_in;
+
     const int64_t t_begin = (int64_t)split * a.tokens_per_split;
     int64_t t_end = t_begin + a.tokens_per_split;
     if (t_end > a.M) t_end = a.M;
-    const int stages = t_end > t_begin ? (int)((t_end - t_begin + kT - 1) / kT) : 0;
+    const int stages = t_end > t_begin ? (int)((t_end - t_begin + kStageK - 1) / kStageK) : 0;
 
-    const bool spanA = comp == 2 && OUT_T;   // dZ columns j*D + g
-    const bool spanB = comp == 2 && IN_T;    // X columns k*D + g
-    const bool do_db = a.want_db && comp == 1 && kt == 0;
+    // first source column of each side (plain: column of row 0; strided: the
+    // vector holding row 0's column)
+    const int colA = SPAN_A ? j0 * D + (D >= 16 ? (g & ~7) : 0) : g * bo + j0;
+    const int colB = SPAN_B ? k0 * D + (D >= 16 ? (g & ~7) : 0) : g * bi + k0;
+    // element of a strided vector holding row t (t < kPerVec): (t * D + g) & 7
+    const int gsel = g & 7;
 
-    // wave -> groups and sub-tile
-    const int wg0 = D >= 4 ? wave * T::kGPW : wave / T::kWPG;
-    const int wsub = D >= 4 ? 0 : wave % T::kWPG;
-    const int wj0 = (wsub / T::kWavesK) * WJ, wk0 = (wsub % T::kWavesK) * WK;
-
-    f32x4_t acc[T::kGPW][T::kSubJ][T::kSubK];
+    // per-thread block: side, token block tb, vector column vc; byte offset of
+    // its first token row within a stage
+    uint32_t voff[kIters];
 #pragma unroll
-    for (int g = 0; g < T::kGPW; ++g)
+    for (int q = 0; q < kIters; ++q) {
+        const int bid = (tid + q * kThreads) % kBlk;
+        const bool sideA = bid < kBlkA;
+        const int local = sideA ? bid : bid - kBlkA;
+        const int vcols = sideA ? SA::kVecCols : SB::kVecCols;
+        const int vc = local % vcols, tb = local / vcols;
+        const int ld = sideA ? n_out : n_in;
+        const bool span = sideA ? SPAN_A : SPAN_B;
+        const int col = (sideA ? colA : colB) + (span ? vc * (D <= 8 ? 8 : D) : vc * 8);
+        voff[q] = (uint32_t)(tb * 8) * (uint32_t)ld * 2u + (uint32_t)col * 2u;
+    }
+
+    f32x4_t acc[C::kSubJ][C::kSubK];
 #pragma unroll
-        for (int i = 0; i < T::kSubJ; ++i)
+    for (int i = 0; i < C::kSubJ; ++i)
 #pragma unroll
-            for (int j = 0; j < T::kSubK; ++j) acc[g][i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < C::kSubK; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    uint4 reg[kIters][8];
 
-    uint4 reg[T::kIters][8];
+    const bool do_db = !C2 && a.want_db && kt == 0;
+    // half-row hr = tid + q*256 (q < kDbIters) of the dZ tile: tokens 16*(hr & 1)..+16 of row hr >> 1
+    constexpr int kDbIters = (2 * BJ + kThreads - 1) / kThreads;
+    float dbacc[kDbIters];
+#pragma unroll
+    for (int q = 0; q < kDbIters; ++q) dbacc[q] = 0.f;
 
-    // block id -> (side, source column of its first element, token row block)
-    // side A: rows of dZ; side B: rows of X.  8 consecutive LDS rows per block
-    // in slice mode; 8 consecutive span columns in span mode.
-    auto block_src = [&](int bid, bool &sideA, int64_t &col, int &tb, int &r8) {
-        sideA = bid < T::kBlocksA;
-        const int local = sideA ? bid : bid - T::kBlocksA;
-        tb = local % (kT / 8);
-        r8 = (local / (kT / 8)) * 8;             // first LDS row (slice) / span column (span)
-        if (sideA) {
-            if (spanA) col = j0 * D + r8;                              // span columns
-            else col = (int64_t)(r8 / J) * a.bo + j0 + (r8 % J);       // group r8/J, rows
-        } else {
-            if (spanB) col = k0 * D + r8;
-            else col = (int64_t)(r8 / K) * a.bi + k0 + (r8 % K);
-        }
-    };
-
+    // ---- global -> registers: stage s's 8x8 blocks.  The buffer is rebased at
+    // the stage's first token and ends at the split's end, so tokens past it
+    // read as zero.
     auto fetch = [&](int s) {
-        const int64_t tok0 = t_begin + (int64_t)s * kT;
+        const int64_t tok = t_begin + (int64_t)s * kStageK;
+        const int64_t left = t_end - tok;
+        const uint32_t rows = (uint32_t)(left < kStageK ? left : kStageK);
+        const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(a.dZ + tok * n_out, rows * (uint32_t)n_out * 2u);
+        const __amdgpu_buffer_rsrc_t rB = buffer_rsrc(a.X + tok * n_in, rows * (uint32_t)n_in * 2u);
 #pragma unroll
-        for (int it = 0; it < T::kIters; ++it) {
-            const int bid = tid + it * kThreads;
-            if (bid < T::kBlocks) {
-                bool sideA; int64_t col; int tb, r8;
-                block_src(bid, sideA, col, tb, r8);
-                const uint16_t *base = sideA ? a.dZ : a.X;
-                const int64_t ld = sideA ? a.n_out : a.n_in;
+        for (int q = 0; q < kIters; ++q) {
+            const int bid = tid + q * kThreads;
+            if (kBlk % kThreads == 0 || bid < kBlk) {
+                const bool sideA = bid < kBlkA;
+                const uint32_t ld2 = (uint32_t)(sideA ? n_out : n_in) * 2u;
 #pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    const int64_t m = tok0 + tb * 8 + t;
-                    reg[it][t] = m < t_end ? ldg16(base + m * ld + col) : make_uint4(0, 0, 0, 0);
+                for (int t = 0; t < 8; ++t) reg[q][t] = bload16(sideA ? rA : rB, voff[q] + t * ld2, 0);
+            }
+        }
+    };
+
+    // ---- registers -> LDS: transpose each block; a strided block keeps only
+    // the group's residue
+    auto stash = [&](uint16_t *buf) {
+#pragma unroll
+        for (int q = 0; q < kIters; ++q) {
+            const int bid = tid + q * kThreads;
+            if (kBlk % kThreads == 0 || bid < kBlk) {
+                const bool sideA = bid < kBlkA;
+                const int local = sideA ? bid : bid - kBlkA;
+                const int vcols = sideA ? SA::kVecCols : SB::kVecCols;
+                const int vc = local % vcols, tb = local / vcols;
+                uint16_t *dst = buf + (sideA ? 0 : BJ * kStageK);
+                const bool span = sideA ? SPAN_A : SPAN_B;
+                if (!span) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        *reinterpret_cast<uint4 *>(dst + lds_off(vc * 8 + e, tb)) = column_of(reg[q], e);
+                } else {
+                    constexpr int kpv = D <= 8 ? 8 / D : 1;
+#pragma unroll
+                    for (int t = 0; t < kpv; ++t)
+                        *reinterpret_cast<uint4 *>(dst + lds_off(vc * kpv + t, tb)) =
+                            column_uniform(reg[q], ((t * D) & 7) + (D <= 8 ? g : gsel));
                 }
             }
         }
     };
 
-    auto stash = [&]() {
+    const int wj0 = (wave / C::kWavesK) * C::WJ, wk0 = (wave % C::kWavesK) * C::WK;
+    auto compute = [&](const uint16_t *buf) {
+        const uint16_t *bufB = buf + BJ * kStageK;
+        const int lr = lane & 15, lc = lane >> 4;
+        bf16x8_t af[C::kSubJ];
 #pragma unroll
-        for (int it = 0; it < T::kIters; ++it) {
-            const int bid = tid + it * kThreads;
-            if (bid < T::kBlocks) {
-                bool sideA; int64_t col; int tb, r8;
-                block_src(bid, sideA, col, tb, r8);
-                const bool span = sideA ? spanA : spanB;
-                const int rows_per_group = sideA ? J : K;
-                uint16_t *dst = sideA ? ldsA : ldsB;
+        for (int i = 0; i < C::kSubJ; ++i)
+            af[i] = *reinterpret_cast<const bf16x8_t *>(buf + lds_off(wj0 + i * 16 + lr, lc));
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    int row;
-                    if (span) {
-                        const int c = r8 + e;            // span column: group c % D, index c / D
-                        row = (c % D) * rows_per_group + c / D;
-                    } else {
-                        row = r8 + e;
-                    }
-                    *reinterpret_cast<uint4 *>(dst + row * kRowT + tb * 8) = column_of(reg[it], e);
-                }
-            }
-        }
-    };
-
-    // db: threads sum whole LDS rows of the dZ tile (comp 1: row = g*J + j, slice mode)
-    constexpr int kDbRows = (T::kRowsA + kThreads - 1) / kThreads;
-    float dbacc[kDbRows];
+        for (int j = 0; j < C::kSubK; ++j) {
+            const bf16x8_t bf = *reinterpret_cast<const bf16x8_t *>(bufB + lds_off(wk0 + j * 16 + lr, lc));
 #pragma unroll
-    for (int q = 0; q < kDbRows; ++q) dbacc[q] = 0.f;
-
-    auto compute = [&]() {
-        const int kq = (lane >> 4) * 8;
-#pragma unroll
-        for (int gg = 0; gg < T::kGPW; ++gg) {
-            const int g = wg0 + gg;
-            bf16x8_t bf[T::kSubK];
-#pragma unroll
-            for (int j = 0; j < T::kSubK; ++j)
-                bf[j] = *reinterpret_cast<const bf16x8_t *>(
-                    ldsB + (g * K + wk0 + j * 16 + (lane & 15)) * kRowT + kq);
-#pragma unroll
-            for (int i = 0; i < T::kSubJ; ++i) {
-                const bf16x8_t af = *reinterpret_cast<const bf16x8_t *>(
-                    ldsA + (g * J + wj0 + i * 16 + (lane & 15)) * kRowT + kq);
-#pragma unroll
-                for (int j = 0; j < T::kSubK; ++j)
-                    acc[gg][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[j], acc[gg][i][j], 0, 0, 0);
-            }
+            for (int i = 0; i < C::kSubJ; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
         }
         if (do_db) {
 #pragma unroll
-            for (int q = 0; q < kDbRows; ++q) {
-                const int row = tid + q * kThreads;
-                if (row < T::kRowsA) {
+            for (int q = 0; q < kDbIters; ++q) {
+                const int hr = tid + q * kThreads, row = hr >> 1, h = hr & 1;
+                if (hr < 2 * BJ) {
 #pragma unroll
-                    for (int v = 0; v < kT / 8; ++v) {
-                        const uint4 w = *reinterpret_cast<const uint4 *>(ldsA + row * kRowT + v * 8);
+                    for (int c = 0; c < 2; ++c) {
+                        const uint4 w = *reinterpret_cast<const uint4 *>(buf + lds_off(row, 2 * h + c));
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const uint32_t d = word(w, e);
-                            dbacc[q] += bf16_to_f32((uint16_t)(d & 0xffffu)) + bf16_to_f32((uint16_t)(d >> 16));
-                        }
+                        for (int e = 0; e < 8; ++e) dbacc[q] += unpack_bf16(word_of(w, e >> 1), e & 1);
                     }
                 }
             }
         }
     };
 
-    if (stages > 0) fetch(0);
-    for (int s = 0; s < stages; ++s) {
+    auto buf = [&](int s) -> uint16_t * { return lds + (s & 1) * C::kStageElems; };
+    if (stages > 0) {
+        fetch(0);
+        stash(buf(0));
+        if (stages > 1) fetch(1);
         __syncthreads();
-        stash();
-        __syncthreads();
-        if (s + 1 < stages) fetch(s + 1);
-        compute();
+        int s = 0;
+        for (; s + 2 < stages; ++s) {
+            stash(buf(s + 1));
+            fetch(s + 2);
+            compute(buf(s));
+            __syncthreads();
+        }
+        if (s + 1 < stages) {
+            stash(buf(s + 1));
+            compute(buf(s));
+            __syncthreads();
+            ++s;
+        }
+        compute(buf(s));
     }
 
-    // partial sums -> workspace [split][comp-1][g][j][k]
-    const int64_t per_comp = (int64_t)D * a.bo * a.bi;
-    float *dst = a.part + ((int64_t)split * 2 + (comp - 1)) * per_comp;
+    // partial sums -> workspace [split][comp][g][j][k]
+    const int64_t per_comp = (int64_t)(a.bo * a.bi) * (int64_t)(a.n_out / a.bo);
+    float *dst = a.part + ((int64_t)split * 2 + (C2 ? 1 : 0)) * per_comp + (int64_t)g * bo * bi;
 #pragma unroll
-    for (int gg = 0; gg < T::kGPW; ++gg) {
-        const int g = wg0 + gg;
+    for (int i = 0; i < C::kSubJ; ++i)
 #pragma unroll
-        for (int i = 0; i < T::kSubJ; ++i)
+        for (int j = 0; j < C::kSubK; ++j)
 #pragma unroll
-            for (int j = 0; j < T::kSubK; ++j)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int64_t jj = j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
-                    const int64_t kk = k0 + wk0 + j * 16 + (lane & 15);
-                    dst[(g * a.bo + jj) * a.bi + kk] = acc[gg][i][j][v];
-                }
-    }
-    if (do_db) {
-#pragma unroll
-        for (int q = 0; q < kDbRows; ++q) {
-            const int row = tid + q * kThreads;
-            if (row < T::kRowsA) {
-                const int g = row / J, j = row % J;
-                a.part_db[(int64_t)split * a.n_out + g * a.bo + j0 + j] = dbacc[q];
+            for (int v = 0; v < 4; ++v) {
+                const int jj = j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
+                const int kk = k0 + wk0 + j * 16 + (lane & 15);
+                dst[(int64_t)jj * bi + kk] = acc[i][j][v];
             }
+    if (do_db) {
+        // the two halves of each row sit in adjacent lanes
+#pragma unroll
+        for (int q = 0; q < kDbIters; ++q) {
+            const int hr = tid + q * kThreads;
+            const float other = __shfl_xor(dbacc[q], 1);
+            if (hr < 2 * BJ && (hr & 1) == 0)
+                a.part_db[(int64_t)split * n_out + g * bo + j0 + (hr >> 1)] = dbacc[q] + other;
         }
     }
+}
+
+template <int D, int BJ, int BK, bool IN_T, bool OUT_T>
+__global__ void __launch_bounds__(kThreads, 2) dyad_dw_mfma(DwArgs a) {
+    using C = DwCfg<D, BJ, BK, IN_T, OUT_T>;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[C::kLds];
+    // workgroup -> (split, component, group, j tile, k tile): XCD x = w % 8
+    // takes splits x, x + 8, ...; within an XCD, one split's tiles are adjacent
+    const int w = blockIdx.x, x = w & 7, i = w >> 3;
+    const int tiles = 2 * D * a.tiles_j * a.tiles_k;
+    const int split = x + 8 * (i / tiles);
+    int t = i % tiles;
+    const int kt = t % a.tiles_k; t /= a.tiles_k;
+    const int jt = t % a.tiles_j; t /= a.tiles_j;
+    const int g = t % D, comp = t / D;
+    if (split >= a.splits) return;
+    if (comp == 0) dw_tile<D, BJ, BK, IN_T, OUT_T, false>(a, smem, split, g, jt, kt);
+    else dw_tile<D, BJ, BK, IN_T, OUT_T, true>(a, smem, split, g, jt, kt);
 }
 
 // Adds the splits in order 0..S-1 and writes dW1, dW2 (and db) in bf16.
@@ -280,56 +302,54 @@ __global__ void __launch_bounds__(256) dyad_dw_reduce(const float *part, const f
             s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
         }
         uint2 o;
-        o.x = f32_to_bf16(s.x) | ((uint32_t)f32_to_bf16(s.y) << 16);
-        o.y = f32_to_bf16(s.z) | ((uint32_t)f32_to_bf16(s.w) << 16);
+        o.x = pack_bf16(s.x, s.y);
+        o.y = pack_bf16(s.z, s.w);
         uint16_t *out = is_db ? db + idx : (idx < per_comp ? dW1 + idx : dW2 + (idx - per_comp));
         *reinterpret_cast<uint2 *>(out) = o;
     }
 }
 
 struct DwPlan {
-    int J, K, tiles_j, tiles_k, splits;
+    int BJ, BK, tiles_j, tiles_k, splits, splits_per_xcd;
     int64_t tokens_per_split;
-    bool ok;
 };
 
-DwPlan plan_for(const DwPass &p, int J, int K) {
-    DwPlan pl{};
-    pl.J = J; pl.K = K;
-    pl.tiles_j = (int)(p.bo / J);
-    pl.tiles_k = (int)(p.bi / K);
-    const int64_t tiles = 2 * (int64_t)pl.tiles_j * pl.tiles_k;
-    // enough workgroups to cover 256 CUs about twice; each split a multiple of kT tokens
-    int64_t want = (512 + tiles - 1) / tiles;
-    const int64_t max_splits = (p.M + kT - 1) / kT;
-    if (want > max_splits) want = max_splits;
-    if (want < 1) want = 1;
-    int64_t tps = (p.M + want - 1) / want;
-    tps = (tps + kT - 1) / kT * kT;
-    if (tps < kT) tps = kT;
-    pl.tokens_per_split = tps;
-    pl.splits = (int)((p.M + tps - 1) / tps);
-    if (pl.splits < 1) pl.splits = 1;
-    pl.ok = true;
-    return pl;
-}
+// Tile candidates (BJ, BK) for n_dyad D, widest first.
+struct Cand { int D, BJ, BK; };
+constexpr Cand kCands[] = {
+    {1, 128, 128}, {1, 128, 64}, {1, 64, 128}, {1, 64, 64},
+    {2, 128, 128}, {2, 128, 64}, {2, 64, 128}, {2, 64, 64},
+    {4, 128, 192}, {4, 192, 128}, {4, 128, 128}, {4, 128, 64}, {4, 64, 128}, {4, 64, 64},
+    {8, 64, 64}, {16, 64, 64},
+};
 
 bool choose(const DwPass &p, DwPlan &pl) {
-    if (p.dtype != kBF16) return false;
-    struct Cand { int D, J, K; };
-    static const Cand cands[] = {
-        {1, 256, 128}, {1, 128, 256}, {2, 128, 128}, {4, 128, 64}, {4, 64, 128},
-        {8, 64, 64}, {16, 64, 32}, {16, 32, 64},
-    };
-    for (const Cand &c : cands)
-        if (c.D == p.D && p.bo % c.J == 0 && p.bi % c.K == 0) {
-            pl = plan_for(p, c.J, c.K);
-            return true;
-        }
+    if (p.dtype != kBF16 || p.M <= 0) return false;
+    // 32-bit buffer offsets within one 32-token stage
+    if ((int64_t)kStageK * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;
+    for (const Cand &c : kCands) {
+        if (c.D != p.D || p.bo % c.BJ || p.bi % c.BK) continue;
+        pl.BJ = c.BJ; pl.BK = c.BK;
+        pl.tiles_j = (int)(p.bo / c.BJ);
+        pl.tiles_k = (int)(p.bi / c.BK);
+        // splits: a multiple of 8 (one token range per XCD and round), about two
+        // workgroups per CU, each split at least four stages long
+        const int64_t tiles = 2 * p.D * (int64_t)pl.tiles_j * pl.tiles_k;
+        int64_t splits = 8 * ((512 + 8 * tiles - 1) / (8 * tiles));
+        const int64_t max_splits = (p.M + 4 * kStageK - 1) / (4 * kStageK);
+        if (splits > max_splits) splits = max_splits;
+        if (splits < 1) splits = 1;
+        int64_t tps = (p.M + splits - 1) / splits;
+        tps = (tps + kStageK - 1) / kStageK * kStageK;
+        pl.tokens_per_split = tps;
+        pl.splits = (int)((p.M + tps - 1) / tps);
+        pl.splits_per_xcd = (pl.splits + 7) / 8;
+        return true;
+    }
     return false;
 }
 
-template <int D, int J, int K, int WJ, int WK, bool IN_T, bool OUT_T>
+template <int D, int BJ, int BK, bool IN_T, bool OUT_T>
 hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     DwArgs a;
     a.M = p.M; a.n_in = p.n_in; a.n_out = p.n_out; a.bi = p.bi; a.bo = p.bo;
@@ -338,10 +358,12 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.part = static_cast<float *>(p.ws);
     a.part_db = a.part + (int64_t)pl.splits * 2 * p.D * p.bo * p.bi;
     a.tokens_per_split = pl.tokens_per_split;
-    a.tiles_j = pl.tiles_j; a.tiles_k = pl.tiles_k; a.splits = pl.splits;
+    a.tiles_j = pl.tiles_j; a.tiles_k = pl.tiles_k;
+    a.splits = pl.splits; a.splits_per_xcd = pl.splits_per_xcd;
     a.want_db = p.db != nullptr;
-    const int64_t blocks = 2 * (int64_t)pl.tiles_j * pl.tiles_k * pl.splits;
-    dyad_dw_mfma<D, J, K, WJ, WK, IN_T, OUT_T><<<(unsigned)blocks, kThreads, 0, s>>>(a);
+    const int64_t tiles = 2 * p.D * (int64_t)pl.tiles_j * pl.tiles_k;
+    const int64_t blocks = 8 * tiles * pl.splits_per_xcd;
+    dyad_dw_mfma<D, BJ, BK, IN_T, OUT_T><<<(unsigned)blocks, kThreads, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t per_comp = p.D * p.bo * p.bi;
@@ -358,16 +380,13 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
 
 template <bool IN_T, bool OUT_T>
 hipError_t launch_dw_variant(const DwPass &p, const DwPlan &pl, hipStream_t s) {
-#define DYAD_DW_CASE(D_, J_, K_, WJ_, WK_) \
-    if (p.D == D_ && pl.J == J_ && pl.K == K_) return launch_dw_cfg<D_, J_, K_, WJ_, WK_, IN_T, OUT_T>(p, pl, s);
-    DYAD_DW_CASE(1, 256, 128, 128, 64)
-    DYAD_DW_CASE(1, 128, 256, 64, 128)
-    DYAD_DW_CASE(2, 128, 128, 64, 128)
-    DYAD_DW_CASE(4, 128, 64, 128, 64)
-    DYAD_DW_CASE(4, 64, 128, 64, 128)
-    DYAD_DW_CASE(8, 64, 64, 64, 64)
-    DYAD_DW_CASE(16, 64, 32, 64, 32)
-    DYAD_DW_CASE(16, 32, 64, 32, 64)
+#define DYAD_DW_CASE(D_, J_, K_) \
+    if (p.D == D_ && pl.BJ == J_ && pl.BK == K_) return launch_dw_cfg<D_, J_, K_, IN_T, OUT_T>(p, pl, s);
+    DYAD_DW_CASE(1, 128, 128) DYAD_DW_CASE(1, 128, 64) DYAD_DW_CASE(1, 64, 128) DYAD_DW_CASE(1, 64, 64)
+    DYAD_DW_CASE(2, 128, 128) DYAD_DW_CASE(2, 128, 64) DYAD_DW_CASE(2, 64, 128) DYAD_DW_CASE(2, 64, 64)
+    DYAD_DW_CASE(4, 128, 192) DYAD_DW_CASE(4, 192, 128) DYAD_DW_CASE(4, 128, 128)
+    DYAD_DW_CASE(4, 128, 64) DYAD_DW_CASE(4, 64, 128) DYAD_DW_CASE(4, 64, 64)
+    DYAD_DW_CASE(8, 64, 64) DYAD_DW_CASE(16, 64, 64)
 #undef DYAD_DW_CASE
     return hipErrorNotSupported;
 }

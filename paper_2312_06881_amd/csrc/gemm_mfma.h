@@ -37,18 +37,10 @@
 
 #include <type_traits>
 
-#include "dyad_device.h"
 #include "dyad_internal.h"
+#include "mfma_common.h"
 
 namespace dyad {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
-typedef __attribute__((ext_vector_type(4))) float f32x4_t;
-typedef __attribute__((ext_vector_type(2))) float f32x2_t;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
-
-constexpr int kStageK = 32;   // k per stage and per MFMA (v_mfma_f32_16x16x32_bf16)
 
 struct GemmArgs {
     int64_t M, Kin, Nout, bk, bn, D;
@@ -58,131 +50,6 @@ struct GemmArgs {
     int tiles_n;        // output tiles per token panel
     int tiles_total;
 };
-
-// ---- buffer loads ------------------------------------------------------------
-
-// Word 3 of a raw buffer resource on gfx9-family parts: 32-bit data, no swizzle.
-constexpr int kBufferWord3 = 0x00020000;
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kBufferWord3);
-}
-
-// 16 bytes at base + voff + soff; zero when voff lies past the buffer's range.
-__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ uint4 ldg16(const uint16_t *p) { return *reinterpret_cast<const uint4 *>(p); }
-
-// ---- register shuffles ---------------------------------------------------------
-
-// Word w (0..3) of a 16-byte vector, w known at compile time after unrolling.
-__device__ __forceinline__ uint32_t word_of(const uint4 &v, int w) {
-    const uint32_t lo = (w & 1) ? v.y : v.x;
-    const uint32_t hi = (w & 1) ? v.w : v.z;
-    return (w & 2) ? hi : lo;
-}
-
-// v_perm_b32 selector placing the 16-bit value at byte offset b of {hi:lo} in
-// the low half and the one at byte offset c in the high half.
-__host__ __device__ constexpr uint32_t perm_sel(int b, int c) {
-    return (uint32_t)b | ((uint32_t)(b + 1) << 8) | ((uint32_t)c << 16) | ((uint32_t)(c + 1) << 24);
-}
-
-// Residue R (compile time) of 8 consecutive k values held in D consecutive
-// 16-byte vectors (input column k*D + r, residue fastest), as one 16-byte
-// vector of the 8 values.  Element e of the span sits in vector e / 8, word
-// (e % 8) / 2, half e % 2; each output word takes two such halves with one
-// v_perm_b32.
-template <int D, int R>
-__device__ __forceinline__ uint4 deinterleave(const uint4 (&v)[D]) {
-    uint32_t o[4];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-        const int e0 = (2 * w) * D + R, e1 = (2 * w + 1) * D + R;
-        const uint32_t a = word_of(v[e0 >> 3], (e0 & 7) >> 1);   // holds e0
-        const uint32_t b = word_of(v[e1 >> 3], (e1 & 7) >> 1);   // holds e1
-        // bytes 0-3 of {b:a} are a, bytes 4-7 are b
-        o[w] = __builtin_amdgcn_perm(b, a, perm_sel((e0 & 1) * 2, 4 + (e1 & 1) * 2));
-    }
-    return make_uint4(o[0], o[1], o[2], o[3]);
-}
-
-// Residue r, a value uniform across the workgroup, of the span: one branch per
-// residue, each a compile-time shuffle.
-template <int D, int R = 0>
-__device__ __forceinline__ uint4 deinterleave_uniform(const uint4 (&v)[D], int r) {
-    if constexpr (R + 1 < D) {
-        if (r != R) return deinterleave_uniform<D, R + 1>(v, r);
-    }
-    return deinterleave<D, R>(v);
-}
-
-// Every residue of the span into its own LDS slab (slab R at dst + R * slab).
-template <int D, int R = 0>
-__device__ __forceinline__ void deinterleave_all(const uint4 (&v)[D], uint16_t *dst, int slab) {
-    *reinterpret_cast<uint4 *>(dst + R * slab) = deinterleave<D, R>(v);
-    if constexpr (R + 1 < D) deinterleave_all<D, R + 1>(v, dst, slab);
-}
-
-// Column e (0..7) of an 8x8 block of bf16 given as 8 rows of 8: the 8 row values, packed.
-__device__ __forceinline__ uint4 column_of(const uint4 (&r)[8], int e) {
-    uint32_t o[4];
-    const uint32_t sel = (e & 1) ? perm_sel(2, 6) : perm_sel(0, 4);
-#pragma unroll
-    for (int p = 0; p < 4; ++p)
-        o[p] = __builtin_amdgcn_perm(word_of(r[2 * p + 1], e >> 1), word_of(r[2 * p], e >> 1), sel);
-    return make_uint4(o[0], o[1], o[2], o[3]);
-}
-
-// ---- epilogue math -------------------------------------------------------------
-
-// Two fp32 values as packed bf16, round to nearest even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-    const f32x2_t v = {a, b};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
-}
-
-__device__ __forceinline__ float unpack_bf16(uint32_t w, int half) {
-    return __uint_as_float(half ? (w & 0xffff0000u) : (w << 16));
-}
-
-// Standard normal CDF and density at x.  erfc(|x|/sqrt 2) uses the rational
-// approximation 7.1.26 of Abramowitz & Stegun (absolute error below 1.5e-7 in
-// erf), far below the bf16 rounding of the result; it shares exp(-x^2/2) with
-// the density.
-__device__ __forceinline__ void normal_cdf_pdf(float x, float &cdf, float &pdf) {
-    const float z = fabsf(x) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
-    const float poly =
-        t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f),
-                 0.254829592f);
-    const float e = __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);   // exp(-x^2 / 2)
-    const float tail = 0.5f * poly * e;                                      // P(N > |x|)
-    cdf = x >= 0.f ? 1.f - tail : tail;
-    pdf = 0.3989422804014327f * e;
-}
-
-// ---- layout helpers --------------------------------------------------------------
-
-// bf16 element offset of 16-byte chunk c (0..3) of LDS row `row` (rows of 32
-// bf16, 64 bytes).  The chunk position is XORed with (row >> 1) & 3, which
-// spreads the 16-byte fragment reads of 16 consecutive rows at one chunk over
-// distinct banks (measured on gfx950: full LDS read bandwidth, where unswizzled
-// 64-byte rows run at half of it).
-__device__ __forceinline__ int lds_off(int row, int c) {
-    return row * kStageK + ((c ^ (row >> 1)) & 3) * 8;
-}
-
-// Tile index of workgroup w, with consecutive tiles (one token panel's column
-// tiles, then the next panel's) placed on one XCD: the hardware deals
-// workgroups round-robin over the 8 XCDs, each with its own L2.
-__device__ __forceinline__ int xcd_tile(int w, int total) {
-    const int q = total >> 3, r = total & 7, x = w & 7, i = w >> 3;
-    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
-}
 
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
 struct GemmCfg {
