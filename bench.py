@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--only", default="",
                     help="run just this call (e.g. IT:fc1.fwd) --steps times, for counter collection")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("CALL", "FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs of --only CALL (FETCH_SIZE, WRITE_SIZE) into "
+                         "profiles/traffic_<workload>.json")
     return ap.parse_args()
 
 
@@ -117,6 +120,9 @@ def build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args, *args.summarize_pmc)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
                                    "(the multi-GPU design is described, not built)",
@@ -317,6 +323,67 @@ def cpu_baseline(wl, tokens):
             "kind": "oracle", "seconds": round(dt, 2),
             "sample": f"{wl.name}, Dyad-IT only, every layer fwd + dX + dW + db on {Ms} of {wl.M} "
                       f"tokens (fp64 plain loops, OpenMP); input generation included"}
+
+
+COPY_BYTES = 256 << 20   # the plain copy --only runs beside the call, for counter calibration
+
+
+def _pmc_rows(run_dir):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    return list(csv.DictReader(open(files[0])))
+
+
+def _per_launch(rows, counter):
+    """(average KiB per launch of the call's kernels, KiB the copy kernel read/wrote, launches)."""
+    rows = [r for r in rows if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    copies = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+    big = max(int(r["Grid_Size"]) for r in copies)
+    copy_kib = [float(r["Counter_Value"]) for r in copies if int(r["Grid_Size"]) == big]
+    # the call's kernels sit between consecutive copies: one launch = the dispatches of one gap
+    launches, cur = [], 0.0
+    for r in rows:
+        if "copyBuffer" in r["Kernel_Name"]:
+            if int(r["Grid_Size"]) == big and cur > 0:
+                launches.append(cur)
+                cur = 0.0
+        else:
+            cur += float(r["Counter_Value"])
+    if cur > 0:
+        launches.append(cur)
+    return sum(launches) / len(launches), sum(copy_kib) / len(copy_kib), len(launches)
+
+
+def summarize_pmc(args, call, fetch_dir, write_dir):
+    """HBM bytes per launch of `call`: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by
+    what the same counter reads for a plain 256 MiB copy run beside it."""
+    f_kib, f_copy, n_f = _per_launch(_pmc_rows(fetch_dir), "FETCH_SIZE")
+    w_kib, w_copy, n_w = _per_launch(_pmc_rows(write_dir), "WRITE_SIZE")
+    f_scale = COPY_BYTES / (f_copy * 1024)
+    w_scale = COPY_BYTES / (w_copy * 1024)
+    fetch = f_kib * 1024 * f_scale
+    write = w_kib * 1024 * w_scale
+    path = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+    rec = {}
+    if os.path.exists(path):
+        rec = json.load(open(path))
+    if rec.get("source_hash") != kernel_source_hash():
+        rec = {"source_hash": kernel_source_hash(), "calls": {}}
+    rec["calls"][call] = {"hbm_bytes_per_launch": round(fetch + write), "fetch_bytes": round(fetch),
+                          "write_bytes": round(write), "fetch_raw_kib": round(f_kib, 1),
+                          "write_raw_kib": round(w_kib, 1), "fetch_scale": round(f_scale, 4),
+                          "write_scale": round(w_scale, 4), "launches": [n_f, n_w],
+                          "commands": [f"rocprofv3 --pmc {c} --output-format csv -d <dir>/{c} -o run -- "
+                                       f"python -u bench.py --only {call} --steps 5" for c in ("FETCH_SIZE", "WRITE_SIZE")]
+                          + [f"python bench.py --summarize-pmc {call} <dir>/FETCH_SIZE <dir>/WRITE_SIZE"]}
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as fh:
+        json.dump(rec, fh, indent=1, sort_keys=True)
+    print(json.dumps({call: rec["calls"][call]}))
 
 
 def kernel_source_hash():

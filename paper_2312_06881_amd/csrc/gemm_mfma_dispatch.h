@@ -47,8 +47,11 @@ template <int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     if (p.bk % kStageK != 0) return hipErrorNotSupported;
     constexpr int BM = D >= 8 ? 64 : 128;
+    // with an output transpose a 128 x 256 tile's D slabs need one workgroup per
+    // CU; 64 x 256 keeps two, which measures faster
+    constexpr int BM256 = OUT_T ? 64 : BM;
     if constexpr (!OUT_T || (256 / D >= 16 && D < 16))
-        if (p.bn % 256 == 0) return launch_tile<BM, 256, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
+        if (p.bn % 256 == 0) return launch_tile<BM256, 256, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
     if constexpr (!OUT_T || (192 % D == 0 && (192 / D) % 16 == 0))
         if (p.bn % 192 == 0) return launch_tile<BM, 192, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
     if constexpr (!OUT_T || 128 / D >= 16)
