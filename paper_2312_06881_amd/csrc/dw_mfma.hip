@@ -61,34 +61,39 @@ __device__ __forceinline__ uint4 column_uniform(const uint4 (&r)[8], int e) {
 // columns k of the tile), 32 tokens each.
 //   plain:  source column first + row, for row in [0, rows)
 //   strided (SPAN): source column (first + row) * D + g
-template <int D, bool SPAN, int ROWS>
+template <int D, bool SPAN, int ROWS, int NSUB>
 struct Side {
     // k values (LDS rows) per loaded 16-byte vector, and vectors per 8 tokens
     static constexpr int kPerVec = SPAN ? (D <= 8 ? 8 / D : 1) : 8;
-    static constexpr int kVecCols = ROWS / kPerVec;              // vector columns per token row
-    static constexpr int kBlocks = kVecCols * (kStageK / 8);     // 8x8 blocks per stage
+    static constexpr int kVecCols = ROWS / kPerVec;                     // vector columns per token row
+    static constexpr int kBlocks = kVecCols * (NSUB * kStageK / 8);     // 8x8 blocks per stage
     static_assert(ROWS % kPerVec == 0, "whole vectors per tile");
 };
 
-template <int D, int BJ, int BK, bool IN_T, bool OUT_T>
+// A stage is NSUB consecutive 32-token sub-stages (one MFMA K step each), each
+// stored as its own [BJ + BK][32] LDS tile.
+template <int D, int BJ, int BK, int NSUB>
 struct DwCfg {
     static constexpr int kWavesJ = 2, kWavesK = 2;
     static constexpr int WJ = BJ / kWavesJ, WK = BK / kWavesK;
     static constexpr int kSubJ = WJ / 16, kSubK = WK / 16;
-    static constexpr int kStageElems = (BJ + BK) * kStageK;       // bf16 per LDS stage buffer
+    static constexpr int kTokens = NSUB * kStageK;                // tokens per stage
+    static constexpr int kSubElems = (BJ + BK) * kStageK;         // bf16 per sub-stage tile
+    static constexpr int kStageElems = NSUB * kSubElems;          // bf16 per LDS stage buffer
     static constexpr int kLds = 2 * kStageElems * 2;
-    static constexpr int kMaxBlocks = 2 * (BJ * D + BK * D) / 8 * (kStageK / 8);
+    // one workgroup per CU once the accumulators pass 128 per lane
+    static constexpr int kOcc = (BJ * BK / 256 > 128 || 2 * kLds > 160 * 1024) ? 1 : 2;
     static_assert(WJ % 16 == 0 && WK % 16 == 0, "whole MFMA blocks per wave");
     static_assert(kLds <= 160 * 1024, "LDS budget");
 };
 
-template <int D, int BJ, int BK, bool IN_T, bool OUT_T, bool C2>
+template <int D, int BJ, int BK, int NSUB, bool IN_T, bool OUT_T, bool C2>
 __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, int split, int g, int jt, int kt) {
-    using C = DwCfg<D, BJ, BK, IN_T, OUT_T>;
+    using C = DwCfg<D, BJ, BK, NSUB>;
     constexpr bool SPAN_A = C2 && OUT_T;    // dZ columns j*D + g
     constexpr bool SPAN_B = C2 && IN_T;     // X columns k*D + g
-    using SA = Side<D, SPAN_A, BJ>;
-    using SB = Side<D, SPAN_B, BK>;
+    using SA = Side<D, SPAN_A, BJ, NSUB>;
+    using SB = Side<D, SPAN_B, BK, NSUB>;
     constexpr int kBlkA = SA::kBlocks, kBlk = SA::kBlocks + SB::kBlocks;
     constexpr int kIters = (kBlk + kThreads - 1) / kThreads;
 
@@ -100,7 +105,7 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     const int64_t t_begin = (int64_t)split * a.tokens_per_split;
     int64_t t_end = t_begin + a.tokens_per_split;
     if (t_end > a.M) t_end = a.M;
-    const int stages = t_end > t_begin ? (int)((t_end - t_begin + kStageK - 1) / kStageK) : 0;
+    const int stages = t_end > t_begin ? (int)((t_end - t_begin + C::kTokens - 1) / C::kTokens) : 0;
 
     // first source column of each side (plain: column of row 0; strided: the
     // vector holding row 0's column)
@@ -133,7 +138,7 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     uint4 reg[kIters][8];
 
     const bool do_db = !C2 && a.want_db && kt == 0;
-    // half-row hr = tid + q*256 (q < kDbIters) of the dZ tile: tokens 16*(hr & 1)..+16 of row hr >> 1
+    // half-row hr = tid + q*256 (q < kDbIters) of a sub-stage's dZ tile: tokens 16*(hr & 1)..+16 of row hr >> 1
     constexpr int kDbIters = (2 * BJ + kThreads - 1) / kThreads;
     float dbacc[kDbIters];
 #pragma unroll
@@ -143,9 +148,9 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     // the stage's first token and ends at the split's end, so tokens past it
     // read as zero.
     auto fetch = [&](int s) {
-        const int64_t tok = t_begin + (int64_t)s * kStageK;
+        const int64_t tok = t_begin + (int64_t)s * C::kTokens;
         const int64_t left = t_end - tok;
-        const uint32_t rows = (uint32_t)(left < kStageK ? left : kStageK);
+        const uint32_t rows = (uint32_t)(left < C::kTokens ? left : C::kTokens);
         const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(a.dZ + tok * n_out, rows * (uint32_t)n_out * 2u);
         const __amdgpu_buffer_rsrc_t rB = buffer_rsrc(a.X + tok * n_in, rows * (uint32_t)n_in * 2u);
 #pragma unroll
@@ -171,17 +176,19 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
                 const int local = sideA ? bid : bid - kBlkA;
                 const int vcols = sideA ? SA::kVecCols : SB::kVecCols;
                 const int vc = local % vcols, tb = local / vcols;
-                uint16_t *dst = buf + (sideA ? 0 : BJ * kStageK);
+                // token block tb: sub-stage tb / 4, 16-byte chunk tb % 4 of its rows
+                uint16_t *dst = buf + (tb >> 2) * C::kSubElems + (sideA ? 0 : BJ * kStageK);
+                const int chunk = tb & 3;
                 const bool span = sideA ? SPAN_A : SPAN_B;
                 if (!span) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
-                        *reinterpret_cast<uint4 *>(dst + lds_off(vc * 8 + e, tb)) = column_of(reg[q], e);
+                        *reinterpret_cast<uint4 *>(dst + lds_off(vc * 8 + e, chunk)) = column_of(reg[q], e);
                 } else {
                     constexpr int kpv = D <= 8 ? 8 / D : 1;
 #pragma unroll
                     for (int t = 0; t < kpv; ++t)
-                        *reinterpret_cast<uint4 *>(dst + lds_off(vc * kpv + t, tb)) =
+                        *reinterpret_cast<uint4 *>(dst + lds_off(vc * kpv + t, chunk)) =
                             column_uniform(reg[q], ((t * D) & 7) + (D <= 8 ? g : gsel));
                 }
             }
@@ -189,30 +196,34 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     };
 
     const int wj0 = (wave / C::kWavesK) * C::WJ, wk0 = (wave % C::kWavesK) * C::WK;
-    auto compute = [&](const uint16_t *buf) {
-        const uint16_t *bufB = buf + BJ * kStageK;
-        const int lr = lane & 15, lc = lane >> 4;
-        bf16x8_t af[C::kSubJ];
+    auto compute = [&](const uint16_t *stage) {
 #pragma unroll
-        for (int i = 0; i < C::kSubJ; ++i)
-            af[i] = *reinterpret_cast<const bf16x8_t *>(buf + lds_off(wj0 + i * 16 + lr, lc));
-#pragma unroll
-        for (int j = 0; j < C::kSubK; ++j) {
-            const bf16x8_t bf = *reinterpret_cast<const bf16x8_t *>(bufB + lds_off(wk0 + j * 16 + lr, lc));
+        for (int sub = 0; sub < NSUB; ++sub) {
+            const uint16_t *buf = stage + sub * C::kSubElems;
+            const uint16_t *bufB = buf + BJ * kStageK;
+            const int lr = lane & 15, lc = lane >> 4;
+            bf16x8_t af[C::kSubJ];
 #pragma unroll
             for (int i = 0; i < C::kSubJ; ++i)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
-        }
-        if (do_db) {
+                af[i] = *reinterpret_cast<const bf16x8_t *>(buf + lds_off(wj0 + i * 16 + lr, lc));
 #pragma unroll
-            for (int q = 0; q < kDbIters; ++q) {
-                const int hr = tid + q * kThreads, row = hr >> 1, h = hr & 1;
-                if (hr < 2 * BJ) {
+            for (int j = 0; j < C::kSubK; ++j) {
+                const bf16x8_t bf = *reinterpret_cast<const bf16x8_t *>(bufB + lds_off(wk0 + j * 16 + lr, lc));
 #pragma unroll
-                    for (int c = 0; c < 2; ++c) {
-                        const uint4 w = *reinterpret_cast<const uint4 *>(buf + lds_off(row, 2 * h + c));
+                for (int i = 0; i < C::kSubJ; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
+            }
+            if (do_db) {
 #pragma unroll
-                        for (int e = 0; e < 8; ++e) dbacc[q] += unpack_bf16(word_of(w, e >> 1), e & 1);
+                for (int q = 0; q < kDbIters; ++q) {
+                    const int hr = tid + q * kThreads, row = hr >> 1, h = hr & 1;
+                    if (hr < 2 * BJ) {
+#pragma unroll
+                        for (int c = 0; c < 2; ++c) {
+                            const uint4 w = *reinterpret_cast<const uint4 *>(buf + lds_off(row, 2 * h + c));
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) dbacc[q] += unpack_bf16(word_of(w, e >> 1), e & 1);
+                        }
                     }
                 }
             }
@@ -266,22 +277,30 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     }
 }
 
-template <int D, int BJ, int BK, bool IN_T, bool OUT_T>
-__global__ void __launch_bounds__(kThreads, 2) dyad_dw_mfma(DwArgs a) {
-    using C = DwCfg<D, BJ, BK, IN_T, OUT_T>;
+template <int D, int BJ, int BK, int NSUB, bool IN_T, bool OUT_T>
+__global__ void __launch_bounds__(kThreads, (DwCfg<D, BJ, BK, NSUB>::kOcc)) dyad_dw_mfma(DwArgs a) {
+    using C = DwCfg<D, BJ, BK, NSUB>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::kLds];
-    // workgroup -> (split, component, group, j tile, k tile): XCD x = w % 8
-    // takes splits x, x + 8, ...; within an XCD, one split's tiles are adjacent
-    const int w = blockIdx.x, x = w & 7, i = w >> 3;
+    // workgroup -> (split, component, group, j tile, k tile).  With a multiple
+    // of 8 splits, XCD x = w % 8 takes splits x, x + 8, ... and one split's
+    // tiles are adjacent on it; otherwise splits simply follow each other.
+    const int w = blockIdx.x;
     const int tiles = 2 * D * a.tiles_j * a.tiles_k;
-    const int split = x + 8 * (i / tiles);
-    int t = i % tiles;
+    int split, t;
+    if (a.splits % 8 == 0) {
+        const int x = w & 7, i = w >> 3;
+        split = x + 8 * (i / tiles);
+        t = i % tiles;
+    } else {
+        split = w / tiles;
+        t = w % tiles;
+    }
     const int kt = t % a.tiles_k; t /= a.tiles_k;
     const int jt = t % a.tiles_j; t /= a.tiles_j;
     const int g = t % D, comp = t / D;
     if (split >= a.splits) return;
-    if (comp == 0) dw_tile<D, BJ, BK, IN_T, OUT_T, false>(a, smem, split, g, jt, kt);
-    else dw_tile<D, BJ, BK, IN_T, OUT_T, true>(a, smem, split, g, jt, kt);
+    if (comp == 0) dw_tile<D, BJ, BK, NSUB, IN_T, OUT_T, false>(a, smem, split, g, jt, kt);
+    else dw_tile<D, BJ, BK, NSUB, IN_T, OUT_T, true>(a, smem, split, g, jt, kt);
 }
 
 // Adds the splits in order 0..S-1 and writes dW1, dW2 (and db) in bf16.
@@ -310,46 +329,62 @@ __global__ void __launch_bounds__(256) dyad_dw_reduce(const float *part, const f
 }
 
 struct DwPlan {
-    int BJ, BK, tiles_j, tiles_k, splits, splits_per_xcd;
+    int BJ, BK, NSUB, occ, tiles_j, tiles_k, splits, splits_per_xcd;
     int64_t tokens_per_split;
 };
 
-// Tile candidates (BJ, BK) for n_dyad D, widest first.
-struct Cand { int D, BJ, BK; };
+// Tile candidates for n_dyad D, preferred first: (BJ, BK) weight tile and
+// NSUB 32-token sub-stages per pipeline stage.
+struct Cand { int D, BJ, BK, NSUB; };
 constexpr Cand kCands[] = {
-    {1, 128, 128}, {1, 128, 64}, {1, 64, 128}, {1, 64, 64},
-    {2, 128, 128}, {2, 128, 64}, {2, 64, 128}, {2, 64, 64},
-    {4, 128, 192}, {4, 192, 128}, {4, 128, 128}, {4, 128, 64}, {4, 64, 128}, {4, 64, 64},
-    {8, 64, 64}, {16, 64, 64},
+    {1, 128, 128, 1}, {1, 128, 64, 1}, {1, 64, 128, 1}, {1, 64, 64, 1},
+    {2, 128, 128, 1}, {2, 128, 64, 1}, {2, 64, 128, 1}, {2, 64, 64, 1},
+    {4, 128, 192, 1}, {4, 192, 128, 1}, {4, 128, 128, 1}, {4, 128, 64, 1}, {4, 64, 128, 1}, {4, 64, 64, 1},
+    {8, 64, 64, 1}, {16, 64, 64, 1},
 };
+
+template <int D, int BJ, int BK, int NSUB>
+constexpr int cand_occ() { return DwCfg<D, BJ, BK, NSUB>::kOcc; }
+
+int occ_of(const Cand &c) {
+#define DYAD_DW_OCC(D_, J_, K_, N_) if (c.D == D_ && c.BJ == J_ && c.BK == K_ && c.NSUB == N_) return cand_occ<D_, J_, K_, N_>();
+    DYAD_DW_OCC(4, 128, 192, 1) DYAD_DW_OCC(4, 192, 128, 1)
+#undef DYAD_DW_OCC
+    return 2;
+}
 
 bool choose(const DwPass &p, DwPlan &pl) {
     if (p.dtype != kBF16 || p.M <= 0) return false;
-    // 32-bit buffer offsets within one 32-token stage
-    if ((int64_t)kStageK * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;
     for (const Cand &c : kCands) {
         if (c.D != p.D || p.bo % c.BJ || p.bi % c.BK) continue;
-        pl.BJ = c.BJ; pl.BK = c.BK;
+        const int64_t stage_tokens = (int64_t)kStageK * c.NSUB;
+        // 32-bit buffer offsets within one stage
+        if (stage_tokens * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;
+        pl.BJ = c.BJ; pl.BK = c.BK; pl.NSUB = c.NSUB; pl.occ = occ_of(c);
         pl.tiles_j = (int)(p.bo / c.BJ);
         pl.tiles_k = (int)(p.bi / c.BK);
-        // splits: a multiple of 8 (one token range per XCD and round), about two
-        // workgroups per CU, each split at least four stages long
+        // splits: a multiple of 8 (one token range per XCD and round), enough
+        // workgroups to fill every CU's slots once, each split at least four
+        // stages long
         const int64_t tiles = 2 * p.D * (int64_t)pl.tiles_j * pl.tiles_k;
-        int64_t splits = 8 * ((512 + 8 * tiles - 1) / (8 * tiles));
-        const int64_t max_splits = (p.M + 4 * kStageK - 1) / (4 * kStageK);
+        const int64_t slots = 256 * (int64_t)pl.occ;
+        // enough tiles fill the GPU without splitting the tokens at all
+        int64_t splits = tiles >= slots ? 1 : 8 * ((slots + 8 * tiles - 1) / (8 * tiles));
+        const int64_t max_splits = (p.M + 4 * stage_tokens - 1) / (4 * stage_tokens);
         if (splits > max_splits) splits = max_splits;
         if (splits < 1) splits = 1;
         int64_t tps = (p.M + splits - 1) / splits;
-        tps = (tps + kStageK - 1) / kStageK * kStageK;
+        tps = (tps + stage_tokens - 1) / stage_tokens * stage_tokens;
         pl.tokens_per_split = tps;
         pl.splits = (int)((p.M + tps - 1) / tps);
         pl.splits_per_xcd = (pl.splits + 7) / 8;
+        if (tiles * pl.splits >= ((int64_t)1 << 31)) return false;
         return true;
     }
     return false;
 }
 
-template <int D, int BJ, int BK, bool IN_T, bool OUT_T>
+template <int D, int BJ, int BK, int NSUB, bool IN_T, bool OUT_T>
 hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     DwArgs a;
     a.M = p.M; a.n_in = p.n_in; a.n_out = p.n_out; a.bi = p.bi; a.bo = p.bo;
@@ -362,8 +397,8 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.splits = pl.splits; a.splits_per_xcd = pl.splits_per_xcd;
     a.want_db = p.db != nullptr;
     const int64_t tiles = 2 * p.D * (int64_t)pl.tiles_j * pl.tiles_k;
-    const int64_t blocks = 8 * tiles * pl.splits_per_xcd;
-    dyad_dw_mfma<D, BJ, BK, IN_T, OUT_T><<<(unsigned)blocks, kThreads, 0, s>>>(a);
+    const int64_t blocks = pl.splits % 8 == 0 ? 8 * tiles * pl.splits_per_xcd : tiles * pl.splits;
+    dyad_dw_mfma<D, BJ, BK, NSUB, IN_T, OUT_T><<<(unsigned)blocks, kThreads, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t per_comp = p.D * p.bo * p.bi;
@@ -380,13 +415,14 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
 
 template <bool IN_T, bool OUT_T>
 hipError_t launch_dw_variant(const DwPass &p, const DwPlan &pl, hipStream_t s) {
-#define DYAD_DW_CASE(D_, J_, K_) \
-    if (p.D == D_ && pl.BJ == J_ && pl.BK == K_) return launch_dw_cfg<D_, J_, K_, IN_T, OUT_T>(p, pl, s);
-    DYAD_DW_CASE(1, 128, 128) DYAD_DW_CASE(1, 128, 64) DYAD_DW_CASE(1, 64, 128) DYAD_DW_CASE(1, 64, 64)
-    DYAD_DW_CASE(2, 128, 128) DYAD_DW_CASE(2, 128, 64) DYAD_DW_CASE(2, 64, 128) DYAD_DW_CASE(2, 64, 64)
-    DYAD_DW_CASE(4, 128, 192) DYAD_DW_CASE(4, 192, 128) DYAD_DW_CASE(4, 128, 128)
-    DYAD_DW_CASE(4, 128, 64) DYAD_DW_CASE(4, 64, 128) DYAD_DW_CASE(4, 64, 64)
-    DYAD_DW_CASE(8, 64, 64) DYAD_DW_CASE(16, 64, 64)
+#define DYAD_DW_CASE(D_, J_, K_, N_)                                             \
+    if (p.D == D_ && pl.BJ == J_ && pl.BK == K_ && pl.NSUB == N_)                \
+        return launch_dw_cfg<D_, J_, K_, N_, IN_T, OUT_T>(p, pl, s);
+    DYAD_DW_CASE(1, 128, 128, 1) DYAD_DW_CASE(1, 128, 64, 1) DYAD_DW_CASE(1, 64, 128, 1) DYAD_DW_CASE(1, 64, 64, 1)
+    DYAD_DW_CASE(2, 128, 128, 1) DYAD_DW_CASE(2, 128, 64, 1) DYAD_DW_CASE(2, 64, 128, 1) DYAD_DW_CASE(2, 64, 64, 1)
+    DYAD_DW_CASE(4, 128, 192, 1) DYAD_DW_CASE(4, 192, 128, 1) DYAD_DW_CASE(4, 128, 128, 1)
+    DYAD_DW_CASE(4, 128, 64, 1) DYAD_DW_CASE(4, 64, 128, 1) DYAD_DW_CASE(4, 64, 64, 1)
+    DYAD_DW_CASE(8, 64, 64, 1) DYAD_DW_CASE(16, 64, 64, 1)
 #undef DYAD_DW_CASE
     return hipErrorNotSupported;
 }

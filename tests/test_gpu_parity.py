@@ -11,6 +11,7 @@ import torch
 import oracle
 import paper_2312_06881_amd as dy
 from workloads import OPT125M, OPT350M, TINY, layer_inputs
+from workloads import draw as _draw
 from tests.parity_util import assert_close, to64
 
 pytestmark = pytest.mark.gpu
@@ -33,6 +34,10 @@ SMALL = [  # (n_in, n_out, n_dyad, M)
     (192, 96, 3, 50),     # odd n_dyad, block widths 64 and 32
     (40, 24, 8, 33),      # block widths 5 and 3
 ]
+
+
+def workloads_draw(name, shape, std):
+    return _draw(name, shape, std, "bf16")
 
 
 def case_id(c):
@@ -276,3 +281,37 @@ def test_backward_dw_many_splits(shape, variant):
     assert_close(dw1, r1, "bf16", "dW1")
     assert_close(dw2, r2, "bf16", "dW2")
     assert_close(db, rb, "bf16", "db")
+
+
+# ---- width/block sweep and the wide layer, full size, sampled ---------------------
+
+@pytest.mark.parametrize("d,D", [(1024, 16), (2048, 8), (4096, 4), (8192, 2)],
+                         ids=lambda v: str(v))
+def test_sweep_dt_sampled(d, D):
+    """Dyad-DT feed-forward at sweep shapes: fc1 d -> 4d, fc2 4d -> d (GELU' on fc2's dX), M = 16384."""
+    for li, (n_in, n_out, act) in enumerate(((d, 4 * d, "none"), (4 * d, d, "gelu"))):
+        banner("sweep", d, D, n_in, n_out)
+        check_full_layer(n_in, n_out, D, 16384, "DT", act, seed_offset=li)
+
+
+@pytest.mark.parametrize("M", [16, 256, 32768])
+def test_wide_it_forward(M):
+    """Wide layer 8192 -> 32768, n_dyad 16, Dyad-IT forward; small-M rows checked in full."""
+    n_in, n_out, D = 8192, 32768, 16
+    banner("wide_forward", M)
+    X = workloads_draw("X", (M, n_in), 1.0)
+    W1 = workloads_draw("W1", (D, n_out // D, n_in // D), 0.02)
+    W2 = workloads_draw("W2", (D, n_out // D, n_in // D), 0.02)
+    b = workloads_draw("bias", (n_out,), 0.02)
+    y = dy.forward(gpu(X), gpu(W1), gpu(W2), gpu(b), variant="IT")
+    torch.cuda.synchronize()
+    rows = sample_rows(M, 24, 5) if M > 256 else np.arange(M)
+    f64 = lambda t: t.to(torch.float64).numpy()  # noqa: E731
+    ref = oracle.forward("IT", n_in, n_out, D, X[rows].to(torch.float64).numpy(), f64(W1), f64(W2), f64(b))
+    assert_close(y[rows], ref, "bf16", "Y rows")
+
+
+def test_wide_it_backward_sampled():
+    """Wide layer 8192 -> 32768, n_dyad 16, Dyad-IT dX and dW at M = 4096 tokens, sampled."""
+    banner("wide_backward")
+    check_full_layer(8192, 32768, 16, 4096, "IT", "none")
