@@ -17,8 +17,10 @@ template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W
 hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
     GemmArgs a;
-    // buffer offsets are 32-bit: one token panel of the input and one weight tensor must fit
-    if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || 2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
+    // buffer offsets are 32-bit: one token panel of the input and of the output,
+    // and one weight tensor, must fit
+    if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 2 >= ((int64_t)1 << 31) ||
+        2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
         return hipErrorNotSupported;
     a.M = p.M; a.Kin = p.Kin; a.Nout = p.Nout; a.bk = p.bk; a.bn = p.bn; a.D = p.D;
     a.in = static_cast<const uint16_t *>(p.in);

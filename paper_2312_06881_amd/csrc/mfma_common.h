@@ -106,20 +106,40 @@ __device__ __forceinline__ float unpack_bf16(uint32_t w, int half) {
     return __uint_as_float(half ? (w & 0xffff0000u) : (w << 16));
 }
 
-// Standard normal CDF and density at x.  erfc(|x|/sqrt 2) uses the rational
-// approximation 7.1.26 of Abramowitz & Stegun (absolute error below 1.5e-7 in
-// erf), far below the bf16 rounding of the result; it shares exp(-x^2/2) with
-// the density.
-__device__ __forceinline__ void normal_cdf_pdf(float x, float &cdf, float &pdf) {
-    const float z = fabsf(x) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
+// Upper tail P(N > |x|) of the standard normal, and exp(-x^2/2), which the
+// density shares.  erfc(|x|/sqrt 2) uses the rational approximation 7.1.26 of
+// Abramowitz & Stegun (absolute error below 1.5e-7 in erf, far below the bf16
+// rounding of the results); the halving of erfc is folded into the polynomial.
+__device__ __forceinline__ float normal_tail(float x, float &e) {
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, fabsf(x), 1.0f));
     const float poly =
-        t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f),
-                 0.254829592f);
-    const float e = __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);   // exp(-x^2 / 2)
-    const float tail = 0.5f * poly * e;                                      // P(N > |x|)
-    cdf = x >= 0.f ? 1.f - tail : tail;
-    pdf = 0.3989422804014327f * e;
+        t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 0.5f * 1.061405429f, 0.5f * -1.453152027f), 0.5f * 1.421413741f),
+                         0.5f * -0.284496736f),
+                 0.5f * 0.254829592f);
+    e = __builtin_amdgcn_exp2f(x * (x * -0.72134752044448170f));   // 2^(-x^2 log2(e) / 2)
+    return poly * e;
+}
+
+// GELU(x) = x Phi(x); below zero Phi(x) is the tail itself, which keeps the
+// relative accuracy of small negative outputs.
+__device__ __forceinline__ float gelu(float x) {
+    float e;
+    const float xt = x * normal_tail(x, e);
+    return x >= 0.f ? x - xt : xt;
+}
+
+// GELU'(x) = Phi(x) + x phi(x), phi(x) = exp(-x^2/2) / sqrt(2 pi).
+__device__ __forceinline__ float gelu_grad(float x) {
+    float e;
+    const float tail = normal_tail(x, e);
+    const float cdf = x >= 0.f ? 1.f - tail : tail;
+    return fmaf(x * e, 0.3989422804014327f, cdf);
+}
+
+// 16 bytes to base + voff; dropped when voff lies past the buffer's range.
+__device__ __forceinline__ void bstore16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint4 v) {
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, (int)voff, 0, 0);
 }
 
 // ---- layout helpers --------------------------------------------------------------
