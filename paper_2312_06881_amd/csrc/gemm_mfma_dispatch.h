@@ -5,12 +5,13 @@
 
 namespace dyad {
 
-// Workgroups per CU: two when both the tile's LDS and its registers fit twice
-// (two caps a wave at 256 VGPRs, so accumulators above 128 per lane need one).
+// Workgroups per CU: two 4-wave workgroups when both the tile's LDS and its
+// registers fit twice (two caps a wave at 256 VGPRs, so accumulators above 128
+// per lane need one); an 8-wave workgroup runs alone.
 template <class C>
 constexpr int occupancy() {
     const int acc_per_lane = C::WM * C::WN / 64;
-    return ((160 * 1024) / C::kLds >= 2 && acc_per_lane <= 128) ? 2 : 1;
+    return (C::kThreads <= 256 && (160 * 1024) / C::kLds >= 2 && acc_per_lane <= 128) ? 2 : 1;
 }
 
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
@@ -41,13 +42,47 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Widest column tile that stays inside one output block; with an output
+// Tile choice.  Every tile stays inside one output block; with an output
 // transpose every residue must get a multiple of 16 columns.  A BlockTrans
 // stage with an output transpose stages one A slab per residue, so the token
 // tile shrinks as n_dyad grows to keep both stage buffers in LDS.
+//
+// Large batches (at least one 8-wave workgroup per CU) first try 8-wave tiles,
+// chosen by what the epilogue costs (measured on gfx950 at OPT-125m feed-forward
+// shapes, n_dyad 4): with a plain or bias epilogue 256 x 192 (4 x 2 waves of
+// 64 x 96); with GELU' (input gradient) 128 x 384 (2 x 4 waves of 64 x 96);
+// with GELU after an output transpose 256 x 256 (2 x 4 waves of 128 x 64).
+// Otherwise 4-wave tiles, two workgroups per CU.
+// LDS bytes of a tile (as GemmCfg lays it out), without instantiating it
+constexpr int gemm_lds(int BM, int BN, int WGM, int D, bool OUT_T) {
+    const int operands = 2 * ((OUT_T ? D : 1) * BM * kStageK + BN * kStageK) * 2;
+    const int epi = 2 * (WGM * 16) * (BN + 4) * 4;
+    return operands > epi ? operands : epi;
+}
+
+template <int BM, int BN, int WGM, int D, bool OUT_T>
+constexpr bool tile_ok() {
+    return (!OUT_T || (BN % D == 0 && (BN / D) % 16 == 0)) && gemm_lds(BM, BN, WGM, D, OUT_T) <= 160 * 1024;
+}
+
 template <int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     if (p.bk % kStageK != 0) return hipErrorNotSupported;
+    auto enough = [&](int bm, int bn_tile) { return ((p.M + bm - 1) / bm) * (p.Nout / bn_tile) >= 256; };
+    if constexpr (D <= 4) {
+        if (p.epilogue == kEpiBias) {
+            if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
+                if (p.bn % 192 == 0 && enough(256, 192)) return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
+        } else if (p.epilogue == kEpiGeluGrad) {
+            if constexpr (tile_ok<128, 384, 2, D, OUT_T>())
+                if (p.bn % 384 == 0 && enough(128, 384)) return launch_tile<128, 384, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+            if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
+                if (p.bn % 192 == 0 && enough(256, 192)) return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
+        } else if constexpr (OUT_T && !W_T) {
+            if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+                if (p.bn % 256 == 0 && enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+        }
+    }
     constexpr int BM = D >= 8 ? 64 : 128;
     // with an output transpose a 128 x 256 tile's D slabs need one workgroup per
     // CU; 64 x 256 keeps two, which measures faster
