@@ -55,10 +55,6 @@ struct DwArgs {
     int want_db;
 };
 
-typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
-typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4;
-typedef __attribute__((address_space(3))) unsigned char lds_u8;
-
 constexpr int kDwLdsBudget = 160 * 1024;
 
 // Workgroup shape: WJN x WKN waves, each a WJ x WK block of 16 x 16 MFMA
@@ -118,9 +114,6 @@ struct DwSide {
     static_assert(kKind != 2 || NG == D, "a strided chunk feeds every group");
 };
 
-// Offset that every buffer range check rejects: the load reads zero.
-constexpr uint32_t kNoLoad = 0x80000000u;
-
 // Eight bf16 at base + voff + 2*D*e (e = 0..7), packed into 16 bytes.
 template <int D>
 __device__ __forceinline__ uint4 load_strided8(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
@@ -153,14 +146,6 @@ __device__ __forceinline__ void stash_pieces(const uint4 *v, unsigned char *dst,
     else if constexpr (NJ == 4) *reinterpret_cast<uint2 *>(p) = make_uint2(o[0], o[1]);
     else *reinterpret_cast<uint32_t *>(p) = o[0];
     if constexpr (R + 1 < D) stash_pieces<D, NJ, R + 1>(v, dst, step);
-}
-
-// MFMA operand (8 tokens of one column per lane) from token-major LDS rows:
-// two transpose reads, tokens t..t+3 and t+4..t+7.
-__device__ __forceinline__ bf16x8_t frag_tr(const lds_u8 *p, int pitch) {
-    const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)p);
-    const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(p + 4 * pitch));
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // Load slots of one side: global byte offsets (within a stage's rows) and LDS

@@ -37,23 +37,14 @@
 
 #include <type_traits>
 
-#include "dyad_internal.h"
-#include "mfma_common.h"
+#include "gemm_common.h"
 
 namespace dyad {
 
-struct GemmArgs {
-    int64_t M, Kin, Nout, bk, bn, D;
-    const uint16_t *in, *W1, *W2, *bias, *h_in;
-    uint16_t *out, *h_out;
-    int epilogue;
-    int tiles_n;        // output tiles per token panel
-    int tiles_total;
-};
 
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
 struct GemmCfg {
-    static constexpr int kWaves = WGM * WGN;
+    static constexpr int kWaves = WGM * WGN, kWGN = WGN;
     static constexpr int kThreads = 64 * kWaves;
     static constexpr int WM = BM / WGM, WN = BN / WGN;
     static constexpr int kSubM = WM / 16, kSubN = WN / 16;
@@ -341,108 +332,7 @@ dyad_gemm_mfma(GemmArgs a) {
         __syncthreads();
     }
 
-    // ---- epilogue: per 16-row MFMA block row, accumulators -> LDS (fp32, in
-    // the tile's internal column order, so 16 lanes write 16 consecutive
-    // words) -> real column order on the way out -> bias / GELU / GELU' ->
-    // bf16 -> coalesced 16-byte stores.  Block rows alternate between two
-    // staging buffers, so one barrier per block row suffices.  Bias and the
-    // stashed pre-activations are loaded ahead of use (the latter one block row
-    // ahead), so no global load latency sits between a block row's LDS round
-    // trip and its stores.
-    constexpr int kG8 = BN / 8;                          // 8-column groups per row
-    constexpr int kGroups = C::kEpiRows * kG8;
-    constexpr int kQ = (kGroups + T - 1) / T;            // groups per thread and block row
-    constexpr bool kRagged = kGroups % T != 0;
-    constexpr int kBiasQ = T % kG8 == 0 ? 1 : kQ;        // passes with distinct columns
-    const bool grad = a.epilogue == kEpiGeluGrad;
-    const bool act = a.epilogue == kEpiBiasGelu;
-    const bool bias = a.bias != nullptr && !grad;
-    const bool keep_h = act && a.h_out != nullptr;
-    // The tile's rows as buffers: rows past the batch read zero and drop stores.
-    const uint32_t rows_t = (uint32_t)(rows_left < BM ? rows_left : BM);
-    const uint32_t o_bytes = rows_t * (uint32_t)a.Nout * 2u;
-    const __amdgpu_buffer_rsrc_t rO = buffer_rsrc(a.out + m0 * a.Nout, o_bytes);
-    const uint16_t *hbase = grad ? a.h_in : a.h_out;
-    const __amdgpu_buffer_rsrc_t rH = buffer_rsrc((hbase ? hbase : a.out) + m0 * a.Nout, o_bytes);
-    const uint32_t row16 = 16u * (uint32_t)a.Nout * 2u;  // bytes between block rows
-
-    uint32_t voE[kQ];
-    int c8of[kQ], erof[kQ];
-#pragma unroll
-    for (int q = 0; q < kQ; ++q) {
-        const int gidx = tid + q * T;
-        erof[q] = gidx / kG8;
-        c8of[q] = (gidx % kG8) * 8;
-        const uint32_t row = (uint32_t)((erof[q] / 16) * C::WM + (erof[q] % 16));
-        voE[q] = (row * (uint32_t)a.Nout + (uint32_t)(n0 + c8of[q])) * 2u;
-    }
-    uint4 bq[kBiasQ];
-    if (bias) {
-#pragma unroll
-        for (int q = 0; q < kBiasQ; ++q) bq[q] = ldg16(a.bias + n0 + c8of[q]);
-    }
-    uint4 hq[2][kQ];
-    if (grad) {
-#pragma unroll
-        for (int q = 0; q < kQ; ++q) hq[0][q] = bload16(rH, voE[q], 0);
-    }
-
-#pragma unroll
-    for (int i = 0; i < C::kSubM; ++i) {
-        float *ldsE = reinterpret_cast<float *>(smem) + (i & 1) * C::kEpiElems;
-#pragma unroll
-        for (int j = 0; j < C::kSubN; ++j) {
-            const int col = wn0 + j * 16 + (lane & 15);
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int er = (wave / WGN) * 16 + (lane >> 4) * 4 + v;
-                ldsE[er * C::kEpiPitch + col] = acc[i][j][v];
-            }
-        }
-        __syncthreads();
-        if (grad && i + 1 < C::kSubM) {
-#pragma unroll
-            for (int q = 0; q < kQ; ++q) hq[(i + 1) & 1][q] = bload16(rH, voE[q] + (uint32_t)(i + 1) * row16, 0);
-        }
-#pragma unroll
-        for (int q = 0; q < kQ; ++q) {
-            if (kRagged && tid + q * T >= kGroups) break;
-            const float *rowE = ldsE + erof[q] * C::kEpiPitch;
-            const int c8 = c8of[q];
-            float x[8];
-            if constexpr (OUT_T) {
-                // real column c8 + e sits at internal column internal_col(c8 + e)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) x[e] = rowE[internal_col(c8 + e)];
-            } else {
-                const float4 lo = *reinterpret_cast<const float4 *>(rowE + c8);
-                const float4 hi = *reinterpret_cast<const float4 *>(rowE + c8 + 4);
-                x[0] = lo.x; x[1] = lo.y; x[2] = lo.z; x[3] = lo.w;
-                x[4] = hi.x; x[5] = hi.y; x[6] = hi.z; x[7] = hi.w;
-            }
-            const uint32_t vo = voE[q] + (uint32_t)i * row16;
-            if (grad) {
-                const uint4 h = hq[i & 1][q];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) x[e] *= gelu_grad(unpack_bf16(word_of(h, e >> 1), e & 1));
-            } else {
-                if (bias) {
-                    const uint4 b = bq[kBiasQ == 1 ? 0 : q];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) x[e] += unpack_bf16(word_of(b, e >> 1), e & 1);
-                }
-                if (act) {
-                    if (keep_h)
-                        bstore16(rH, vo, make_uint4(pack_bf16(x[0], x[1]), pack_bf16(x[2], x[3]),
-                                                    pack_bf16(x[4], x[5]), pack_bf16(x[6], x[7])));
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) x[e] = gelu(x[e]);
-                }
-            }
-            bstore16(rO, vo, make_uint4(pack_bf16(x[0], x[1]), pack_bf16(x[2], x[3]), pack_bf16(x[4], x[5]),
-                                        pack_bf16(x[6], x[7])));
-        }
-    }
+    gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0);
 }
 
 }  // namespace dyad

@@ -2,6 +2,7 @@
 #pragma once
 
 #include "gemm_mfma.h"
+#include "gemm_mfma2.h"
 
 namespace dyad {
 
@@ -42,6 +43,46 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     return hipGetLastError();
 }
 
+// Launch of a fused-stage tile (gemm_mfma2.h).
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
+hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
+    using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
+    GemmArgs a;
+    if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 2 >= ((int64_t)1 << 31) ||
+        2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
+        return hipErrorNotSupported;
+    a.M = p.M; a.Kin = p.Kin; a.Nout = p.Nout; a.bk = p.bk; a.bn = p.bn; a.D = p.D;
+    a.in = static_cast<const uint16_t *>(p.in);
+    a.W1 = static_cast<const uint16_t *>(p.W1);
+    a.W2 = static_cast<const uint16_t *>(p.W2);
+    a.bias = static_cast<const uint16_t *>(p.bias);
+    a.h_in = static_cast<const uint16_t *>(p.h_in);
+    a.out = static_cast<uint16_t *>(p.out);
+    a.h_out = static_cast<uint16_t *>(p.h_out);
+    a.epilogue = p.epilogue;
+    const int64_t tiles_m = (p.M + BM - 1) / BM;
+    const int64_t tiles_n = p.Nout / BN;
+    if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    a.tiles_n = (int)tiles_n;
+    a.tiles_total = (int)(tiles_m * tiles_n);
+    dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T><<<a.tiles_total, C::kThreads, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+// Whether a fused-stage tile fits (LDS of Gemm2Cfg, without instantiating it).
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
+constexpr bool tile2_ok() {
+    const int res = OUT_T ? D : 1, cpr = BN / res, wn = BN / WGN;
+    if (OUT_T && (BN % D != 0 || cpr % 16 != 0)) return false;
+    if (wn % cpr != 0 && cpr % wn != 0) return false;
+    if ((BM * 4) % (64 * WGM * WGN) != 0) return false;
+    const int slab = BM * kStageK * 2;
+    const int bbytes = W_T ? kStageK * (BN * 2 + 16) : BN * kStageK * 2;
+    const int operands = 2 * (slab * (1 + res) + 2 * bbytes);
+    const int epi = 2 * (WGM * 16) * (BN + 4) * 4;
+    return (operands > epi ? operands : epi) <= 160 * 1024;
+}
+
 // Tile choice.  Every tile stays inside one output block; with an output
 // transpose every residue must get a multiple of 16 columns.  A BlockTrans
 // stage with an output transpose stages one A slab per residue, so the token
@@ -52,7 +93,8 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
 // shapes, n_dyad 4): with a plain or bias epilogue 256 x 192 (4 x 2 waves of
 // 64 x 96); with GELU' (input gradient) 128 x 384 (2 x 4 waves of 64 x 96);
 // with GELU after an output transpose 256 x 256 (2 x 4 waves of 128 x 64).
-// Otherwise 4-wave tiles, two workgroups per CU.
+// The input gradient without an output transpose takes the fused-stage kernel
+// (gemm_mfma2.h) instead.  Otherwise 4-wave tiles, two workgroups per CU.
 // LDS bytes of a tile (as GemmCfg lays it out), without instantiating it
 constexpr int gemm_lds(int BM, int BN, int WGM, int D, bool OUT_T) {
     const int operands = 2 * ((OUT_T ? D : 1) * BM * kStageK + BN * kStageK) * 2;
@@ -70,6 +112,19 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     if (p.bk % kStageK != 0) return hipErrorNotSupported;
     auto enough = [&](int bm, int bn_tile) { return ((p.M + bm - 1) / bm) * (p.Nout / bn_tile) >= 256; };
     if constexpr (D <= 4) {
+        // the fused-stage kernel (natural-layout weights, transpose reads) wins
+        // for the input gradient without an output transpose
+        if constexpr (W_T && !OUT_T) {
+            if (p.epilogue == kEpiGeluGrad) {
+                if constexpr (tile2_ok<128, 384, 2, 4, D, IN_T, OUT_T, W_T>())
+                    if (p.bn % 384 == 0 && enough(128, 384))
+                        return launch_tile2<128, 384, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+            } else {
+                if constexpr (tile2_ok<256, 192, 4, 2, D, IN_T, OUT_T, W_T>())
+                    if (p.bn % 192 == 0 && enough(256, 192))
+                        return launch_tile2<256, 192, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
+            }
+        }
         if (p.epilogue == kEpiBias) {
             if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
                 if (p.bn % 192 == 0 && enough(256, 192)) return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, W_T>(p, s);

@@ -25,6 +25,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, 
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kBufferWord3);
 }
 
+// Offset that every buffer range check rejects: the load reads zero.
+constexpr uint32_t kNoLoad = 0x80000000u;
+
 // 16 bytes at base + voff + soff; zero when voff lies past the buffer's range.
 __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
@@ -140,6 +143,23 @@ __device__ __forceinline__ float gelu_grad(float x) {
 __device__ __forceinline__ void bstore16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint4 v) {
     const u32x4_t w = {v.x, v.y, v.z, v.w};
     __builtin_amdgcn_raw_buffer_store_b128(w, r, (int)voff, 0, 0);
+}
+
+// ---- transpose reads from LDS ---------------------------------------------------
+
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4_t;
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4;
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+
+// MFMA operand (8 consecutive reduction indices of one column per lane) from
+// LDS rows that run along the columns (one row per reduction index, `pitch`
+// bytes apart): two ds_read_b64_tr_b16, rows t..t+3 and t+4..t+7.  In each
+// 16-lane group, lane s supplies the address of row 8*(group) + s/4, columns
+// 4*(s%4)..+3; lane l gets the 4 rows of column l.
+__device__ __forceinline__ bf16x8_t frag_tr(const lds_u8 *p, int pitch) {
+    const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)p);
+    const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(p + 4 * pitch));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // ---- layout helpers --------------------------------------------------------------
