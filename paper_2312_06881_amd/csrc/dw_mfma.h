@@ -423,6 +423,7 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
 }
 
 // Tile configurations, preferred first: BJ x BK weight tile on WJN x WKN waves.
+// The last, sixteen waves, exists for all-groups items at n_dyad 16.
 #define DYAD_DW_CONFIGS(X)  \
     X(256, 256, 2, 4)       \
     X(192, 256, 2, 4)       \
@@ -432,7 +433,23 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     X(128, 128, 2, 2)       \
     X(128, 64, 2, 2)        \
     X(64, 128, 2, 2)        \
-    X(64, 64, 2, 2)
+    X(64, 64, 2, 2)         \
+    X(128, 128, 4, 4)
+
+// Whether config (BJ, BK, WJN, WKN) has an all-groups layout at n_dyad D.
+inline bool dw_mg_available(int D, int BJ, int BK, int WJN, int WKN) {
+#define DYAD_DW_MG(J_, K_, WJ_, WK_)                                                     \
+    if (BJ == J_ && BK == K_ && WJN == WJ_ && WKN == WK_) switch (D) {                   \
+        case 2: return mg_gb<2, J_, K_, WJ_, WK_>() > 0;                                 \
+        case 4: return mg_gb<4, J_, K_, WJ_, WK_>() > 0;                                 \
+        case 8: return mg_gb<8, J_, K_, WJ_, WK_>() > 0;                                 \
+        case 16: return mg_gb<16, J_, K_, WJ_, WK_>() > 0;                               \
+        default: return false;                                                           \
+    }
+    DYAD_DW_CONFIGS(DYAD_DW_MG)
+#undef DYAD_DW_MG
+    return false;
+}
 
 // Per-variant launchers (one translation unit each).
 hipError_t launch_dw_it(const DwPass &p, const DwPlan &pl, hipStream_t s);

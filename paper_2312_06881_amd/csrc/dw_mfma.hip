@@ -43,13 +43,20 @@ bool choose(const DwPass &p, DwPlan &pl) {
     if (p.D != 1 && p.D != 2 && p.D != 4 && p.D != 8 && p.D != 16) return false;
     // 32-bit buffer offsets within one stage (32 token rows of the wider operand)
     if ((int64_t)kStageK * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;
+    // A strided BlockTrans operand wants a configuration with an all-groups
+    // layout; without one its items read the whole span per group.  At n_dyad
+    // 16 the all-groups tiles (32 x 32 per group) pay off only when both
+    // operands are strided (measured at d = 4096).
+    const bool want_mg = p.D > 1 && (p.in_t || p.out_t) && (p.D < 16 || (p.in_t && p.out_t));
+    for (int pass = want_mg ? 0 : 1; pass < 2; ++pass)
     for (const Cand &c : kCands) {
         if (p.bo % c.BJ || p.bi % c.BK) continue;
+        if (pass == 0 && !dw_mg_available((int)p.D, c.BJ, c.BK, c.WJN, c.WKN)) continue;
         pl.BJ = c.BJ; pl.BK = c.BK; pl.WJN = c.WJN; pl.WKN = c.WKN;
         pl.tiles_j = (int)(p.bo / c.BJ);
         pl.tiles_k = (int)(p.bi / c.BK);
         const int64_t tiles = 2 * p.D * (int64_t)pl.tiles_j * pl.tiles_k;
-        // workgroup slots of the GPU: 256 CUs, one 8-wave or two 4-wave workgroups each
+        // workgroup slots of the GPU: 256 CUs, one workgroup of 8 or more waves or two 4-wave ones each
         const int64_t slots = 256 * (c.WJN * c.WKN >= 8 ? 1 : 2);
         // as many token splits as fit in one round of slots, each at least 8 stages long
         int64_t splits = tiles >= slots ? 1 : slots / tiles;

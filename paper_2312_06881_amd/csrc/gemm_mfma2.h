@@ -47,8 +47,9 @@ struct Gemm2Cfg {
     static constexpr int kLds = kLdsOperands > kLdsEpi ? kLdsOperands : kLdsEpi;
     // load slots per thread and stage
     static constexpr int kRowChunks = BM * (kStageK / 8);               // 16-byte pieces of an A slab
-    static constexpr int kQA1 = kRowChunks / kThreads;
-    static constexpr int kQA2 = IN_T ? kQA1 : kRes * kRowChunks / kThreads;
+    static constexpr int kQA1 = (kRowChunks + kThreads - 1) / kThreads;
+    static constexpr int kUnitsA2 = IN_T ? kRowChunks : kRes * kRowChunks;
+    static constexpr int kQA2 = (kUnitsA2 + kThreads - 1) / kThreads;
     static constexpr int kVA2 = IN_T ? D : 1;                           // an input transpose loads spans
     static constexpr int kUnitsB = W_T ? kStageK * BN / 8 : BN * (kStageK / 8);
     static constexpr int kQB = (kUnitsB + kThreads - 1) / kThreads;
@@ -58,7 +59,7 @@ struct Gemm2Cfg {
     static constexpr int kVB1 = kB1Chunks ? D : 1;
 
     static_assert(BM % (16 * WGM) == 0 && BN % (16 * WGN) == 0, "wave tiles of whole MFMA blocks");
-    static_assert(kRowChunks % kThreads == 0, "A row-chunks spread evenly over the threads");
+    static_assert(kRowChunks % 64 == 0, "whole waves of A row-chunks");
     static_assert(!OUT_T || (BN % D == 0 && kCPR % 16 == 0), "each MFMA column block holds one residue");
     static_assert(WN % kCPR == 0 || kCPR % WN == 0, "waves hold whole residues or parts of one");
     static_assert(kLds <= 160 * 1024, "LDS budget");
@@ -97,22 +98,27 @@ dyad_gemm_mfma2(GemmArgs a) {
     auto real_col = [](int q) -> int { return OUT_T ? (q / C::kCPR) + D * (q % C::kCPR) : q; };
 
     // ---- per-thread offsets, fixed for the tile; a stage adds a scalar offset
+    // (slots past the tile's pieces, small tiles only: load out of range, store nothing)
     uint32_t voA1[C::kQA1], loA1[C::kQA1];
+    bool okA1[C::kQA1], okA2[C::kQA2];
 #pragma unroll
     for (int q = 0; q < C::kQA1; ++q) {
-        const int rc = tid + q * T, row = rc >> 2, c = rc & 3;
-        voA1[q] = (uint32_t)row * (uint32_t)Kin * 2u + (uint32_t)(g1 * bk + c * 8) * 2u;
+        const int rc = (tid + q * T) % C::kRowChunks, row = rc >> 2, c = rc & 3;
+        okA1[q] = tid + q * T < C::kRowChunks;
+        voA1[q] = okA1[q] ? (uint32_t)row * (uint32_t)Kin * 2u + (uint32_t)(g1 * bk + c * 8) * 2u : kNoLoad;
         loA1[q] = (uint32_t)lds_off(row, c) * 2u;
     }
     uint32_t voA2[C::kQA2], loA2[C::kQA2];
 #pragma unroll
     for (int q = 0; q < C::kQA2; ++q) {
-        const int p = tid + q * T;
+        const int p = (tid + q * T) % C::kUnitsA2;
+        okA2[q] = tid + q * T < C::kUnitsA2;
         const int r = IN_T ? 0 : p / C::kRowChunks, rc = p % C::kRowChunks, row = rc >> 2, c = rc & 3;
         const uint32_t rowoff = (uint32_t)row * (uint32_t)Kin * 2u;
         if constexpr (IN_T) voA2[q] = rowoff + (uint32_t)(c * 8 * D) * 2u;            // span of 8 k x D residues
         else voA2[q] = rowoff + (uint32_t)(r * bk + c * 8) * 2u;                      // residue r's input block
         loA2[q] = (uint32_t)(C::kOffA2 + r * C::kSlab) + (uint32_t)lds_off(row, c) * 2u;
+        if (!okA2[q]) voA2[q] = kNoLoad;
     }
     uint32_t voB1[C::kQB1], loB1[C::kQB1], voB2[C::kQB], loB2[C::kQB];
     bool okB1[C::kQB1], okB2[C::kQB];
@@ -192,9 +198,11 @@ dyad_gemm_mfma2(GemmArgs a) {
     // ---- registers -> LDS stage buffer
     auto stash = [&](unsigned char *buf) {
 #pragma unroll
-        for (int q = 0; q < C::kQA1; ++q) *reinterpret_cast<uint4 *>(buf + loA1[q]) = ra1[q];
+        for (int q = 0; q < C::kQA1; ++q)
+            if (C::kRowChunks % T == 0 || okA1[q]) *reinterpret_cast<uint4 *>(buf + loA1[q]) = ra1[q];
 #pragma unroll
         for (int q = 0; q < C::kQA2; ++q) {
+            if (C::kUnitsA2 % T != 0 && !okA2[q]) continue;
             if constexpr (IN_T) {
                 uint4 span[D];
 #pragma unroll

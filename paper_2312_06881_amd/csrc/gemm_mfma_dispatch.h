@@ -75,7 +75,7 @@ constexpr bool tile2_ok() {
     const int res = OUT_T ? D : 1, cpr = BN / res, wn = BN / WGN;
     if (OUT_T && (BN % D != 0 || cpr % 16 != 0)) return false;
     if (wn % cpr != 0 && cpr % wn != 0) return false;
-    if ((BM * 4) % (64 * WGM * WGN) != 0) return false;
+    if ((BM * 4) % 64 != 0) return false;
     const int slab = BM * kStageK * 2;
     const int bbytes = W_T ? kStageK * (BN * 2 + 16) : BN * kStageK * 2;
     const int operands = 2 * (slab * (1 + res) + 2 * bbytes);
@@ -137,6 +137,14 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
             if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
                 if (p.bn % 256 == 0 && enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
         }
+    }
+    // n_dyad 8 and 16 with an output transpose: a 256-column tile gives every
+    // residue 16 or 32 columns; the D input slabs keep the token tile short
+    if constexpr (D >= 8 && OUT_T) {
+        if constexpr (tile2_ok<64, 256, 2, 4, D, IN_T, OUT_T, W_T>())
+            if (p.bn % 256 == 0) return launch_tile2<64, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+        if constexpr (tile2_ok<32, 256, 1, 8, D, IN_T, OUT_T, W_T>())
+            if (p.bn % 256 == 0) return launch_tile2<32, 256, 1, 8, D, IN_T, OUT_T, W_T>(p, s);
     }
     constexpr int BM = D >= 8 ? 64 : 128;
     // with an output transpose a 128 x 256 tile's D slabs need one workgroup per
