@@ -138,6 +138,30 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
                 if (p.bn % 256 == 0 && enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
         }
     }
+    // Blocks of a multiple of 256 columns (OPT-350m, wider layers), from a tile
+    // sweep at d = 1024 (n_dyad 4) and d = 2048 (n_dyad 8)
+    if constexpr (D <= 8) {
+        if (p.bn % 256 == 0) {
+            if constexpr (W_T && (D <= 4 || !OUT_T)) {
+                if constexpr (tile2_ok<128, 256, 2, 4, D, IN_T, OUT_T, W_T>())
+                    if (enough(128, 256)) return launch_tile2<128, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+            } else if constexpr (D == 8 && OUT_T) {
+                if constexpr (tile_ok<128, 256, 2, D, OUT_T>())
+                    if (enough(128, 256)) return launch_tile<128, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+            } else if constexpr (D == 8) {
+                if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+                    if (enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+            } else if (p.epilogue == kEpiBias) {
+                if constexpr (OUT_T) {
+                    if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+                        if (enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
+                } else {
+                    if constexpr (tile_ok<256, 256, 4, D, OUT_T>())
+                        if (enough(256, 256)) return launch_tile<256, 256, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
+                }
+            }
+        }
+    }
     // n_dyad 8 and 16 with an output transpose: a 256-column tile gives every
     // residue 16 or 32 columns; the D input slabs keep the token tile short
     if constexpr (D >= 8 && OUT_T) {
