@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--only", default="",
                     help="run just this call (e.g. IT:fc1.fwd) --steps times, for counter collection")
+    ap.add_argument("--block", default="",
+                    help="instead of the layer step: time an OPT-125m-shaped decoder block fwd+bwd "
+                         "(dense, Dyad FF only, Dyad everywhere) with this variant (IT/OT/DT)")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("CALL", "FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs of --only CALL (FETCH_SIZE, WRITE_SIZE) into "
                          "profiles/traffic_<workload>.json")
@@ -118,6 +121,85 @@ def build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp):
     return out
 
 
+def block_bench(args):
+    """OPT-125m-shaped pre-LN decoder block (d 768, 12 heads, ffn 3072, causal self-attention;
+    batch 8 x 2048 tokens) forward + backward on synthetic bf16 tokens, three ways: dense
+    nn.Linear everywhere, Dyad in the two FF layers only, Dyad in every linear layer (FF and
+    the q / k / v / out projections); plus the FF sub-block alone, dense vs Dyad.  Attention
+    scores and softmax run in fp32 through plain matmuls (contiguous operands)."""
+    import math
+    import torch
+    import torch.nn.functional as F
+    from paper_2312_06881_amd.nn import DyadFF, DyadLinear
+
+    d, ffn, heads, D, B, T = 768, 3072, 12, 4, 8, 2048
+    hd = d // heads
+    v = args.block
+    dev = torch.device("cuda:0")
+    torch.manual_seed(0)
+    bf = torch.bfloat16
+
+    def lin(i, o, dyad):
+        return DyadLinear(i, o, D, v, device=dev) if dyad else torch.nn.Linear(i, o, device=dev, dtype=bf)
+
+    class DenseFF(torch.nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.fc1, self.fc2 = lin(d, ffn, False), lin(ffn, d, False)
+
+        def forward(self, x):
+            return self.fc2(F.gelu(self.fc1(x)))
+
+    mask = torch.full((T, T), float("-inf"), device=dev).triu(1)
+
+    class Block(torch.nn.Module):
+        def __init__(self, attn_dyad, ff_dyad):
+            super().__init__()
+            self.ln1 = torch.nn.LayerNorm(d, device=dev, dtype=bf)
+            self.ln2 = torch.nn.LayerNorm(d, device=dev, dtype=bf)
+            self.q, self.k, self.v, self.o = (lin(d, d, attn_dyad) for _ in range(4))
+            self.ff = DyadFF(d, ffn, D, v, device=dev) if ff_dyad else DenseFF()
+
+        def forward(self, x):
+            h = self.ln1(x)
+            q, k, w = (t.reshape(B, T, heads, hd).transpose(1, 2).float() for t in (self.q(h), self.k(h), self.v(h)))
+            s = torch.matmul(q.contiguous(), k.transpose(-1, -2).contiguous()) / math.sqrt(hd) + mask
+            a = torch.matmul(torch.softmax(s, dim=-1), w.contiguous())
+            x = x + self.o(a.transpose(1, 2).reshape(B, T, d).to(bf).contiguous())
+            return x + self.ff(self.ln2(x))
+
+    x = torch.randn((B, T, d), device=dev, dtype=bf)
+    g = torch.randn((B, T, d), device=dev, dtype=bf)
+
+    def timed(mod, inp):
+        xi = inp.detach().requires_grad_(True)
+        for _ in range(args.warmup):
+            mod(xi).backward(g)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            mod(xi).backward(g)
+        e1.record()
+        torch.cuda.synchronize()
+        return round(e0.elapsed_time(e1) / args.steps, 4)
+
+    res = {"dense": timed(Block(False, False), x), "dyad_ff": timed(Block(False, True), x),
+           "dyad_all": timed(Block(True, True), x),
+           "ff_dense": timed(DenseFF(), x), "ff_dyad": timed(DyadFF(d, ffn, D, v, device=dev), x)}
+    print(json.dumps({
+        "metric": "decoder block forward+backward ms (OPT-125m shape)", "unit": "ms",
+        "higher_is_better": False, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "opt125m_decoder_block", "d": d, "ffn": ffn, "heads": heads, "n_dyad": D,
+                   "variant": v, "batch": B, "seq_len": T},
+        "ms": res,
+        "speedup_vs_dense": {"block_dyad_ff": round(res["dense"] / res["dyad_ff"], 3),
+                             "block_dyad_all": round(res["dense"] / res["dyad_all"], 3),
+                             "ff_only": round(res["ff_dense"] / res["ff_dyad"], 3)},
+    }))
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -128,6 +210,9 @@ def main():
                                    "(the multi-GPU design is described, not built)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.block:
+        block_bench(args)
+        return
     import torch
     import paper_2312_06881_amd as dy
 

@@ -1,0 +1,105 @@
+"""GPU parity of the torch modules (``paper_2312_06881_amd.nn``): autograd through
+the C-ABI against the CPU oracle, on the same seeded inputs as the layer tests."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2312_06881_amd.nn import DyadFF, DyadLinear
+from tests.parity_util import assert_close, to64
+from workloads import layer_inputs
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def banner(*a):
+    print("nn", *a, flush=True)
+
+
+def load_layer(mod, L):
+    with torch.no_grad():
+        mod.w1.copy_(L.W1.to(DEV))
+        mod.w2.copy_(L.W2.to(DEV))
+        if mod.bias is not None:
+            mod.bias.copy_(L.bias.to(DEV))
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_linear_autograd(variant, dtype):
+    """DyadLinear forward and backward (x.grad, W1/W2/bias grads) vs the oracle; a 3-d input."""
+    n_in, n_out, D, B, T = 256, 512, 4, 3, 43          # 129 tokens: a ragged tail
+    M = B * T
+    banner("linear", variant, dtype)
+    L = layer_inputs(n_in, n_out, D, M, dtype)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    mod = DyadLinear(n_in, n_out, D, variant, device=DEV, dtype=tdt)
+    load_layer(mod, L)
+    x = L.X.to(DEV).reshape(B, T, n_in).requires_grad_(True)
+    y = mod(x)
+    assert y.shape == (B, T, n_out)
+    y.backward(L.dZ.to(DEV).reshape(B, T, n_out))
+    torch.cuda.synchronize()
+    ry = oracle.forward(variant, n_in, n_out, D, L.f64("X"), L.f64("W1"), L.f64("W2"), L.f64("bias"))
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, L.f64("dZ"), L.f64("W1"), L.f64("W2"))
+    rw1, rw2, rb = oracle.backward_dw(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"))
+    assert_close(y.reshape(M, n_out), ry, dtype, "y")
+    assert_close(x.grad.reshape(M, n_in), rdx, dtype, "dx")
+    assert_close(mod.w1.grad, rw1, dtype, "dW1")
+    assert_close(mod.w2.grad, rw2, dtype, "dW2")
+    assert_close(mod.bias.grad, rb, dtype, "db")
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+def test_ff_autograd(variant):
+    """DyadFF (fc1 -> GELU -> fc2) forward and backward vs the oracle's layer chain."""
+    d, ffn, D, M = 256, 1024, 4, 130
+    banner("ff", variant)
+    L1 = layer_inputs(d, ffn, D, M, "bf16")
+    L2 = layer_inputs(ffn, d, D, M, "bf16", seed_offset=100)
+    ff = DyadFF(d, ffn, D, variant, device=DEV)
+    load_layer(ff.fc1, L1)
+    load_layer(ff.fc2, L2)
+    x = L1.X.to(DEV).requires_grad_(True)
+    y = ff(x)
+    y.backward(L2.dZ.to(DEV))
+    torch.cuda.synchronize()
+    X = L1.f64("X")
+    ra1, rh1 = oracle.forward(variant, d, ffn, D, X, L1.f64("W1"), L1.f64("W2"), L1.f64("bias"),
+                              act=oracle.ACT_GELU, want_h=True)
+    ry = oracle.forward(variant, ffn, d, D, ra1, L2.f64("W1"), L2.f64("W2"), L2.f64("bias"))
+    rdh = oracle.backward_dx(variant, ffn, d, D, L2.f64("dZ"), L2.f64("W1"), L2.f64("W2"),
+                             act_in=oracle.ACT_GELU, H_in=rh1)
+    r21, r22, rb2 = oracle.backward_dw(variant, ffn, d, D, L2.f64("dZ"), ra1)
+    rdx = oracle.backward_dx(variant, d, ffn, D, rdh, L1.f64("W1"), L1.f64("W2"))
+    r11, r12, rb1 = oracle.backward_dw(variant, d, ffn, D, rdh, X)
+    # each layer rounds its output to bf16 before the next consumes it: the
+    # chain is held to the max-norm bar only
+    for got, ref, what in ((y, ry, "y"), (x.grad, rdx, "dx"), (ff.fc2.w1.grad, r21, "fc2.dW1"),
+                           (ff.fc2.w2.grad, r22, "fc2.dW2"), (ff.fc2.bias.grad, rb2, "fc2.db"),
+                           (ff.fc1.w1.grad, r11, "fc1.dW1"), (ff.fc1.w2.grad, r12, "fc1.dW2"),
+                           (ff.fc1.bias.grad, rb1, "fc1.db")):
+        g = to64(got)
+        err = float(np.abs(g - ref).max() / np.abs(ref).max())
+        assert err <= 2e-2, (what, err)
+
+
+def test_linear_no_bias_and_frozen_weights():
+    """Bias-less layer; weights that do not require grad get none and x.grad is still right."""
+    n_in, n_out, D, M = 512, 256, 8, 70
+    L = layer_inputs(n_in, n_out, D, M, "bf16")
+    mod = DyadLinear(n_in, n_out, D, "OT", bias=False, device=DEV)
+    load_layer(mod, L)
+    mod.w1.requires_grad_(False)
+    mod.w2.requires_grad_(False)
+    x = L.X.to(DEV).requires_grad_(True)
+    mod(x).backward(L.dZ.to(DEV))
+    torch.cuda.synchronize()
+    zero = np.zeros(n_out)
+    ry = oracle.forward("OT", n_in, n_out, D, L.f64("X"), L.f64("W1"), L.f64("W2"), zero)
+    rdx = oracle.backward_dx("OT", n_in, n_out, D, L.f64("dZ"), L.f64("W1"), L.f64("W2"))
+    assert_close(mod(x).detach(), ry, "bf16", "y")
+    assert_close(x.grad, rdx, "bf16", "dx")
+    assert mod.w1.grad is None and mod.w2.grad is None
