@@ -19,9 +19,10 @@
 // order, so the result is bitwise reproducible.
 //
 // Operands in LDS.  A stage holds 32 tokens of both operands in their natural
-// token-major order: one row per token with each group's columns contiguous,
-// rows padded by 16 bytes so that the fragment reads of 16 consecutive tokens
-// fall on distinct banks.  The matrix cores need each lane's 8 values along
+// token-major order: one row per token with each group's columns contiguous.
+// Rows of whole 256-byte blocks have their 32-byte chunks XOR-swizzled by row
+// (tr_swz), other rows are padded by 16 bytes, so that the fragment reads of
+// 16 consecutive tokens spread over the banks.  The matrix cores need each lane's 8 values along
 // the token axis; ds_read_b64_tr_b16 delivers exactly that from token-major
 // rows (four 16-lane groups, each gathering 4 tokens x 16 columns and handing
 // lane l the 4 tokens of column l), so no transpose is done in registers.
@@ -70,12 +71,18 @@ struct DwCfg {
     static_assert(WJ % 16 == 0 && WK % 16 == 0, "whole MFMA tiles per wave");
 };
 
+// LDS row of NG groups of w columns: groups of whole 256-byte blocks are
+// swizzled (tr_swz), other rows keep a 16-byte pad.
+constexpr bool dw_swz(int w) { return (w * 2) % 256 == 0; }
+constexpr int dw_row(int ng, int w) { return ng * w * 2 + (dw_swz(w) ? 0 : 16); }
+
 // Item layout: NG = GA * GB groups on a GA x GB grid of wave blocks, each group
-// JT x KT; LDS rows hold the NG groups' columns side by side plus a 16-byte pad.
+// JT x KT; LDS rows hold the NG groups' columns side by side.
 template <int BJ, int BK, int GA, int GB>
 struct DwLayout {
     static constexpr int NG = GA * GB, JT = BJ / GA, KT = BK / GB;
-    static constexpr int kRowA = NG * JT * 2 + 16, kRowB = NG * KT * 2 + 16;
+    static constexpr bool kSwzA = dw_swz(JT), kSwzB = dw_swz(KT);
+    static constexpr int kRowA = dw_row(NG, JT), kRowB = dw_row(NG, KT);
     static constexpr int kRegionA = kStageK * kRowA;
     static constexpr int kStageBytes = kRegionA + kStageK * kRowB;
 };
@@ -89,7 +96,7 @@ constexpr int mg_gb() {
     for (int gb = 1; gb <= D; gb *= 2) {
         const int ga = D / gb;
         if (WJN % ga || WKN % gb || BJ % (16 * ga) || BK % (16 * gb)) continue;
-        const int bytes = 2 * kStageK * ((gb * BJ * 2 + 16) + (ga * BK * 2 + 16));
+        const int bytes = 2 * kStageK * (dw_row(D, BJ / ga) + dw_row(D, BK / gb));
         if (bytes * DwCfg<BJ, BK, WJN, WKN>::kMinBlocks > kDwLdsBudget) continue;
         const int c = ga * BK + gb * BJ;
         if (c < cost) { cost = c; best = gb; }
@@ -136,23 +143,26 @@ __device__ __forceinline__ void piece_of(const uint4 *v, uint32_t (&o)[NJ / 2]) 
     }
 }
 
-// Every residue's piece of a chunk into its group's columns: piece R at dst + R * step bytes.
-template <int D, int NJ, int R = 0>
-__device__ __forceinline__ void stash_pieces(const uint4 *v, unsigned char *dst, int step) {
+// Every residue's piece of a chunk into its group's columns: piece R at row
+// byte lbyte + R * step of the (swizzled) row at `row`.
+template <int D, int NJ, bool SWZ, int R = 0>
+__device__ __forceinline__ void stash_pieces(const uint4 *v, unsigned char *row, int sw, int lbyte, int step) {
     uint32_t o[NJ / 2];
     piece_of<D, NJ, R>(v, o);
-    unsigned char *p = dst + R * step;
+    // with the swizzle, step is a whole number of 256-byte blocks: the pieces stay step apart
+    unsigned char *p = row + (SWZ ? tr_swz(sw, lbyte) : lbyte) + R * step;
     if constexpr (NJ == 8) *reinterpret_cast<uint4 *>(p) = make_uint4(o[0], o[1], o[2], o[3]);
     else if constexpr (NJ == 4) *reinterpret_cast<uint2 *>(p) = make_uint2(o[0], o[1]);
     else *reinterpret_cast<uint32_t *>(p) = o[0];
-    if constexpr (R + 1 < D) stash_pieces<D, NJ, R + 1>(v, dst, step);
+    if constexpr (R + 1 < D) stash_pieces<D, NJ, SWZ, R + 1>(v, row, sw, lbyte, step);
 }
 
 // Load slots of one side: global byte offsets (within a stage's rows) and LDS
 // byte offsets (within the side's region) of this thread's items.
 template <class S>
 struct DwSlots {
-    uint32_t vo[S::kSlots], lo[S::kSlots];
+    uint32_t vo[S::kSlots], lo[S::kSlots];   // lo: swizzled, or (strided chunks) the row start
+    int lb[S::kSlots], sw[S::kSlots];          // strided chunks: unswizzled row byte and row swizzle
     bool ok[S::kSlots];
     uint4 r[2][S::kSlots][S::kVec];   // two stages in flight
 };
@@ -184,8 +194,9 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
 
     // slot setup of one side: W columns per group starting at w0, groups of bw
     // columns in the input (plain), leading dimension ld
-    auto setup = [&](auto side, auto &sl, int w0, int bw, uint32_t ld, uint32_t region, uint32_t row) {
+    auto setup = [&](auto side, auto swz, auto &sl, int w0, int bw, uint32_t ld, uint32_t region, uint32_t row) {
         using S = decltype(side);
+        constexpr bool SWZ = decltype(swz)::value;
         constexpr int W = S::kPerRow * (S::kKind == 2 ? S::kNJ : 8) / (S::kKind == 0 ? L::NG : 1);
 #pragma unroll
         for (int q = 0; q < S::kSlots; ++q) {
@@ -205,13 +216,16 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
                 lcol = (uint32_t)(S::kNJ * c);
             }
             sl.vo[q] = sl.ok[q] ? (uint32_t)t * ld * 2u + col * 2u : kNoLoad;
-            sl.lo[q] = region + (uint32_t)t * row + lcol * 2u;
+            sl.sw[q] = tr_sw(t);
+            sl.lb[q] = (int)lcol * 2;
+            sl.lo[q] = region + (uint32_t)t * row +
+                       (S::kKind == 2 ? 0u : (uint32_t)(SWZ ? tr_swz(sl.sw[q], (int)lcol * 2) : (int)lcol * 2));
         }
     };
     DwSlots<SA> sa;
     DwSlots<SB> sb;
-    setup(SA{}, sa, j0, bo, n_out, 0u, (uint32_t)L::kRowA);
-    setup(SB{}, sb, k0, bi, n_in, (uint32_t)L::kRegionA, (uint32_t)L::kRowB);
+    setup(SA{}, std::bool_constant<L::kSwzA>{}, sa, j0, bo, n_out, 0u, (uint32_t)L::kRowA);
+    setup(SB{}, std::bool_constant<L::kSwzB>{}, sb, k0, bi, n_in, (uint32_t)L::kRegionA, (uint32_t)L::kRowB);
 
     // ---- global -> registers: stage s into register set P.  Buffers start at
     // the stage's first token and end at the split's end, so tokens past it
@@ -238,21 +252,22 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         fetch_side(SB{}, sb, set, buffer_rsrc(a.X + base * a.n_in, rows * n_in * 2u));
     };
     // ---- registers -> LDS stage buffer
-    auto stash_side = [&](auto side, auto &sl, auto set, unsigned char *buf) {
+    auto stash_side = [&](auto side, auto swz, auto &sl, auto set, unsigned char *buf) {
         using S = decltype(side);
+        constexpr bool SWZ = decltype(swz)::value;
         constexpr int P = decltype(set)::value;
         constexpr int W = S::kKind == 2 ? S::kPerRow * S::kNJ : 0;
 #pragma unroll
         for (int q = 0; q < S::kSlots; ++q) {
             if (S::kItems % T == 0 || sl.ok[q]) {
-                if constexpr (S::kKind == 2) stash_pieces<D, S::kNJ>(sl.r[P][q], buf + sl.lo[q], 2 * W);
+                if constexpr (S::kKind == 2) stash_pieces<D, S::kNJ, SWZ>(sl.r[P][q], buf + sl.lo[q], sl.sw[q], sl.lb[q], 2 * W);
                 else *reinterpret_cast<uint4 *>(buf + sl.lo[q]) = sl.r[P][q][0];
             }
         }
     };
     auto stash = [&](auto set, unsigned char *buf) {
-        stash_side(SA{}, sa, set, buf);
-        stash_side(SB{}, sb, set, buf);
+        stash_side(SA{}, std::bool_constant<L::kSwzA>{}, sa, set, buf);
+        stash_side(SB{}, std::bool_constant<L::kSwzB>{}, sb, set, buf);
     };
 
     f32x4_t acc[C::kSubJ][C::kSubK];
@@ -272,8 +287,10 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     const int wj0 = (wj % kWJG) * C::WJ, wk0 = (wk % kWKG) * C::WK;
     // transpose-read lane offsets: token row 8*(lane/16) + (lane%16)/4, column 4*(lane%4)
     const int trow = 8 * (lane >> 4) + ((lane & 15) >> 2), tcol = 4 * (lane & 3);
-    const uint32_t trA = (uint32_t)(trow * L::kRowA + (gw * L::JT + wj0 + tcol) * 2);
-    const uint32_t trB = (uint32_t)(L::kRegionA + trow * L::kRowB + (gw * L::KT + wk0 + tcol) * 2);
+    // (rows trow and trow + 4 share a swizzle, so frag_tr's second read is one 4-row step on)
+    const int tsw = tr_sw(trow);
+    const int rowA = trow * L::kRowA, colA = (gw * L::JT + wj0 + tcol) * 2;
+    const int rowB = L::kRegionA + trow * L::kRowB, colB = (gw * L::KT + wk0 + tcol) * 2;
     const bf16x8_t ones = {(__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f,
                            (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f};
 
@@ -281,10 +298,12 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         const lds_u8 *b = (const lds_u8 *)buf;
         bf16x8_t af[C::kSubJ];
 #pragma unroll
-        for (int i = 0; i < C::kSubJ; ++i) af[i] = frag_tr(b + trA + i * 32, L::kRowA);
+        for (int i = 0; i < C::kSubJ; ++i)
+            af[i] = frag_tr(b + rowA + (L::kSwzA ? tr_swz(tsw, colA + 32 * i) : colA + 32 * i), L::kRowA);
 #pragma unroll
         for (int j = 0; j < C::kSubK; ++j) {
-            const bf16x8_t bf = frag_tr(b + trB + j * 32, L::kRowB);
+            const bf16x8_t bf =
+                frag_tr(b + rowB + (L::kSwzB ? tr_swz(tsw, colB + 32 * j) : colB + 32 * j), L::kRowB);
 #pragma unroll
             for (int i = 0; i < C::kSubJ; ++i)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
