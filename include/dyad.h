@@ -4,16 +4,22 @@
  * A Dyad layer replaces the dense weight W (n_out x n_in) of y = W x + b
  * (Sec. 2.1) by the sum of two sparse components (Sec. 2.2, Eq. 1), each stored
  * as a 3-D tensor of n_dyad blocks:
- *   W1 = BlockDiag  [n_dyad][n_out/n_dyad][n_in/n_dyad]   (Sec. 2.2.1, Eq. 2)
- *   W2 = BlockTrans [n_dyad][n_out/n_dyad][n_in/n_dyad]   (Sec. 2.2.2, Eq. 5-10)
- * With D = n_dyad, bi = n_in/D, bo = n_out/D, entry W_c[i][j][k] sits in the
- * dense W at (row, col):
+ *   W1 = BlockDiag  [n_dyad][bo][bi]   (Sec. 2.2.1, Eq. 2)
+ *   W2 = BlockTrans [n_dyad][bo][bi]   (Sec. 2.2.2, Eq. 5-10)
+ * With D = n_dyad, bi = ceil(n_in/D), bo = ceil(n_out/D), entry W_c[i][j][k]
+ * sits in the dense W at (row, col):
  *   W1, every variant:  (i*bo + j, i*bi + k)
  *   W2, DYAD_IT:        (i*bo + j, k*D  + i)   input transposed   (Eq. 9-10)
  *   W2, DYAD_OT:        (j*D  + i, i*bi + k)   output transposed  (Sec. 2.4.1, Eq. 11-13)
  *   W2, DYAD_DT:        (j*D  + i, k*D  + i)   both               (Sec. 2.4.2, Eq. 14-16)
  * (The paper's n_in/n_out are per-block sizes; here n_in/n_out are the full
  * layer widths, and bi/bo the per-block ones.)
+ * Widths that n_dyad does not divide are zero-padded up to D*bi and D*bo
+ * (appendix, caveat on rectangular W): the layer acts as the one of widths
+ * D*bi -> D*bo on X with zero columns appended, and only its first n_out
+ * outputs exist.  Entries whose row is >= n_out or whose column is >= n_in
+ * have no effect, and their gradients are zero.  Such widths run on the
+ * general (non-matrix-core) kernels.
  *
  * Layouts: every activation is token-major and row-major: X[M][n_in],
  * Y, H, dZ [M][n_out], dX, H_in [M][n_in]; W1, W2, dW1, dW2 as above; bias and
@@ -49,7 +55,7 @@ typedef enum { DYAD_ACT_NONE = 0, DYAD_ACT_GELU = 1 } dyad_act; /* GELU(x) = x *
 typedef enum {
     DYAD_OK = 0,
     DYAD_ERR_INVALID_ARG = -1, /* unknown enum, size < 0 (M) or <= 0 (n_in, n_out, n_dyad), size overflow, NULL required pointer */
-    DYAD_ERR_SHAPE = -2,       /* n_in or n_out not divisible by n_dyad (the paper pads; padding is the caller's job) */
+    DYAD_ERR_SHAPE = -2,       /* reserved: every shape is accepted (widths n_dyad does not divide are zero-padded) */
     DYAD_ERR_ALIGN = -3,       /* a non-NULL pointer is not 16-byte aligned */
     DYAD_ERR_DTYPE = -4,       /* unknown dtype */
     DYAD_ERR_WORKSPACE = -5,   /* dW workspace NULL or smaller than dyad_dw_workspace_bytes() */

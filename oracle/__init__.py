@@ -89,8 +89,14 @@ def _variant(v) -> int:
 
 
 def _check_shape(n_in, n_out, D):
-    if D <= 0 or n_in % D or n_out % D:
-        raise ValueError(f"n_in={n_in}, n_out={n_out} must be divisible by n_dyad={D}")
+    if D <= 0 or n_in <= 0 or n_out <= 0:
+        raise ValueError(f"n_in={n_in}, n_out={n_out}, n_dyad={D} must be positive")
+
+
+def block_sizes(n_in, n_out, D):
+    """(bi, bo): per-block sizes, each width zero-padded up to a multiple of D
+    (appendix, caveat on rectangular W)."""
+    return -(-n_in // D), -(-n_out // D)
 
 
 def gelu(x: float) -> float:
@@ -113,8 +119,9 @@ def forward(variant, n_in, n_out, D, X, W1, W2, bias=None, act=ACT_NONE, want_h=
     X = _f64(X)
     M = X.shape[0]
     X = _f64(X, (M, n_in))
-    W1 = _f64(W1, (D, n_out // D, n_in // D))
-    W2 = _f64(W2, (D, n_out // D, n_in // D))
+    bi, bo = block_sizes(n_in, n_out, D)
+    W1 = _f64(W1, (D, bo, bi))
+    W2 = _f64(W2, (D, bo, bi))
     b = None if bias is None else _f64(bias, (n_out,))
     Y = np.empty((M, n_out), np.float64)
     H = np.empty((M, n_out), np.float64) if (want_h and act == ACT_GELU) else None
@@ -130,8 +137,9 @@ def backward_dx(variant, n_in, n_out, D, dZ, W1, W2, act_in=ACT_NONE, H_in=None)
     dZ = _f64(dZ)
     M = dZ.shape[0]
     dZ = _f64(dZ, (M, n_out))
-    W1 = _f64(W1, (D, n_out // D, n_in // D))
-    W2 = _f64(W2, (D, n_out // D, n_in // D))
+    bi, bo = block_sizes(n_in, n_out, D)
+    W1 = _f64(W1, (D, bo, bi))
+    W2 = _f64(W2, (D, bo, bi))
     h = None
     if act_in == ACT_GELU:
         if H_in is None:
@@ -151,7 +159,8 @@ def backward_dw(variant, n_in, n_out, D, dZ, X, want_db=True):
     M = dZ.shape[0]
     dZ = _f64(dZ, (M, n_out))
     X = _f64(X, (M, n_in))
-    shp = (D, n_out // D, n_in // D)
+    bi, bo = block_sizes(n_in, n_out, D)
+    shp = (D, bo, bi)
     dW1 = np.empty(shp, np.float64)
     dW2 = np.empty(shp, np.float64)
     db = np.empty((n_out,), np.float64) if want_db else None
@@ -185,7 +194,7 @@ def backward_dw_entries(variant, n_in, n_out, D, dZ, X, comp, i, j, k):
     n = comp.shape[0]
     if not (i.shape[0] == j.shape[0] == k.shape[0] == n):
         raise ValueError("entry index arrays differ in length")
-    bi, bo = n_in // D, n_out // D
+    bi, bo = block_sizes(n_in, n_out, D)
     if n and (comp.min() < 1 or comp.max() > 2 or i.min() < 0 or i.max() >= D or
               j.min() < 0 or j.max() >= bo or k.min() < 0 or k.max() >= bi):
         raise ValueError("entry index out of range")

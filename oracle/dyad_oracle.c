@@ -10,7 +10,7 @@
  * Sec. 2.1 uses the transposed, feature-major convention -- every reshape in the
  * paper acts on the feature index only, so the arithmetic is identical):
  *   D  = n_dyad, the number of blocks per component
- *   n_in, n_out = full layer widths; bi = n_in / D, bo = n_out / D
+ *   n_in, n_out = full layer widths; bi = ceil(n_in / D), bo = ceil(n_out / D)
  *   (bi, bo are what the paper calls n_in, n_out: the size of one block, Sec. 2.2)
  *   X[M][n_in], Y[M][n_out], W1[D][bo][bi] (BlockDiag), W2[D][bo][bi] (BlockTrans)
  *
@@ -32,6 +32,12 @@
  *   - The backward pass is not described in the paper; it is the gradient of
  *     Y = W X + b: dX = W^T dZ, dW_c[i][j][k] = sum_m dZ[m][row] X[m][col],
  *     db = sum_m dZ[m].  Weight gradients are overwritten, not accumulated.
+ *   - Widths that n_dyad does not divide are zero-padded up to the next
+ *     multiple of n_dyad (appendix, caveat on rectangular W): the layer is the
+ *     one of widths D*bi -> D*bo applied to X with zero columns appended, and
+ *     only its first n_out outputs are kept.  An entry whose col is >= n_in
+ *     therefore meets a zero input, and one whose row is >= n_out feeds a
+ *     dropped output: both contribute nothing, and their gradients are zero.
  */
 #include <math.h>
 #include <stddef.h>
@@ -59,6 +65,12 @@ static int64_t entry_col(int variant, int comp, int64_t D, int64_t bi, int64_t i
     if (comp == 1 || variant == ORACLE_OT)
         return i * bi + k;
     return k * D + i;
+}
+
+/* Per-block size of a width zero-padded up to a multiple of D. */
+static int64_t block_size(int64_t n, int64_t D)
+{
+    return (n + D - 1) / D;
 }
 
 /* Standard normal CDF, Phi(x) = erfc(-x / sqrt 2) / 2 (no cancellation for x << 0). */
@@ -93,7 +105,7 @@ void oracle_forward(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t
                     const double *X, const double *W1, const double *W2, const double *bias,
                     int act, double *Y, double *H)
 {
-    const int64_t bi = n_in / D, bo = n_out / D;
+    const int64_t bi = block_size(n_in, D), bo = block_size(n_out, D);
     int64_t m;
 #pragma omp parallel for schedule(static)
     for (m = 0; m < M; ++m) {
@@ -106,9 +118,11 @@ void oracle_forward(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t
             for (int64_t i = 0; i < D; ++i)
                 for (int64_t j = 0; j < bo; ++j)
                     for (int64_t k = 0; k < bi; ++k) {
-                        double w = W[(i * bo + j) * bi + k];
-                        y[entry_row(variant, comp, D, bo, i, j)] +=
-                            w * x[entry_col(variant, comp, D, bi, i, k)];
+                        int64_t row = entry_row(variant, comp, D, bo, i, j);
+                        int64_t col = entry_col(variant, comp, D, bi, i, k);
+                        if (row >= n_out || col >= n_in) /* padded output or zero input */
+                            continue;
+                        y[row] += W[(i * bo + j) * bi + k] * x[col];
                     }
         }
         if (act == ORACLE_ACT_GELU) {
@@ -129,7 +143,7 @@ void oracle_backward_dx(int variant, int64_t n_in, int64_t n_out, int64_t D, int
                         const double *dZ, const double *W1, const double *W2,
                         int act_in, const double *H_in, double *dX)
 {
-    const int64_t bi = n_in / D, bo = n_out / D;
+    const int64_t bi = block_size(n_in, D), bo = block_size(n_out, D);
     int64_t m;
 #pragma omp parallel for schedule(static)
     for (m = 0; m < M; ++m) {
@@ -142,9 +156,11 @@ void oracle_backward_dx(int variant, int64_t n_in, int64_t n_out, int64_t D, int
             for (int64_t i = 0; i < D; ++i)
                 for (int64_t j = 0; j < bo; ++j)
                     for (int64_t k = 0; k < bi; ++k) {
-                        double w = W[(i * bo + j) * bi + k];
-                        dx[entry_col(variant, comp, D, bi, i, k)] +=
-                            w * dz[entry_row(variant, comp, D, bo, i, j)];
+                        int64_t row = entry_row(variant, comp, D, bo, i, j);
+                        int64_t col = entry_col(variant, comp, D, bi, i, k);
+                        if (row >= n_out || col >= n_in) /* no gradient through padding */
+                            continue;
+                        dx[col] += W[(i * bo + j) * bi + k] * dz[row];
                     }
         }
         if (act_in == ORACLE_ACT_GELU)
@@ -173,7 +189,7 @@ void oracle_bias_grad(int64_t n_out, int64_t M, const double *dZ, double *db)
 void oracle_backward_dw(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t M,
                         const double *dZ, const double *X, double *dW1, double *dW2, double *db)
 {
-    const int64_t bi = n_in / D, bo = n_out / D;
+    const int64_t bi = block_size(n_in, D), bo = block_size(n_out, D);
     int64_t t;
 #pragma omp parallel for schedule(static)
     for (t = 0; t < 2 * D * bo; ++t) {
@@ -184,8 +200,9 @@ void oracle_backward_dw(int variant, int64_t n_in, int64_t n_out, int64_t D, int
         for (int64_t k = 0; k < bi; ++k) {
             int64_t col = entry_col(variant, comp, D, bi, i, k);
             double s = 0.0;
-            for (int64_t m = 0; m < M; ++m)
-                s += dZ[m * n_out + row] * X[m * n_in + col];
+            if (row < n_out && col < n_in) /* else the entry touches only padding */
+                for (int64_t m = 0; m < M; ++m)
+                    s += dZ[m * n_out + row] * X[m * n_in + col];
             dW[(i * bo + j) * bi + k] = s;
         }
     }
@@ -202,15 +219,16 @@ void oracle_backward_dw_entries(int variant, int64_t n_in, int64_t n_out, int64_
                                 const int32_t *comp, const int64_t *i, const int64_t *j,
                                 const int64_t *k, double *out)
 {
-    const int64_t bi = n_in / D, bo = n_out / D;
+    const int64_t bi = block_size(n_in, D), bo = block_size(n_out, D);
     int64_t e;
 #pragma omp parallel for schedule(static)
     for (e = 0; e < n_entries; ++e) {
         int64_t row = entry_row(variant, comp[e], D, bo, i[e], j[e]);
         int64_t col = entry_col(variant, comp[e], D, bi, i[e], k[e]);
         double s = 0.0;
-        for (int64_t m = 0; m < M; ++m)
-            s += dZ[m * n_out + row] * X[m * n_in + col];
+        if (row < n_out && col < n_in)
+            for (int64_t m = 0; m < M; ++m)
+                s += dZ[m * n_out + row] * X[m * n_in + col];
         out[e] = s;
     }
 }

@@ -146,11 +146,25 @@ def _check(rc: int):
         raise DyadError(rc, dyad_strerror(rc))
 
 
-def forward(x, w1, w2, bias=None, variant="IT", act="none", stash_h=False):
-    """y = W x + b per token (optionally GELU); returns y, or (y, h) with the pre-activation h."""
+def _width(n, D, b, what):
+    """A layer width: n if given (it must need exactly b blocks of D), else D * b."""
+    if n is None:
+        return D * b
+    if not (D * (b - 1) < n <= D * b):
+        raise ValueError(f"{what}={n} does not fit weight blocks of {b} (n_dyad {D})")
+    return n
+
+
+def forward(x, w1, w2, bias=None, variant="IT", act="none", stash_h=False, n_out=None):
+    """y = W x + b per token (optionally GELU); returns y, or (y, h) with the pre-activation h.
+
+    Weights are [n_dyad, bo, bi]; x is [M, n_in] with n_in padded up to n_dyad * bi.  n_out
+    defaults to n_dyad * bo (or bias's length); a smaller n_out needing the same bo blocks is
+    a zero-padded layer."""
     D, bo, bi = w1.shape
     M, n_in = x.shape
-    n_out = D * bo
+    _width(n_in, D, bi, "n_in")
+    n_out = _width(n_out if n_out is not None or bias is None else bias.shape[0], D, bo, "n_out")
     a = _act(act)
     y = torch.empty((M, n_out), dtype=x.dtype, device=x.device)
     h = torch.empty_like(y) if (stash_h and a == ACT_GELU) else None
@@ -159,11 +173,13 @@ def forward(x, w1, w2, bias=None, variant="IT", act="none", stash_h=False):
     return (y, h) if stash_h else y
 
 
-def backward_dx(dz, w1, w2, variant="IT", act_in="none", h_in=None):
-    """dX = W^T dz per token, times GELU'(h_in) when act_in is "gelu"."""
+def backward_dx(dz, w1, w2, variant="IT", act_in="none", h_in=None, n_in=None):
+    """dX = W^T dz per token, times GELU'(h_in) when act_in is "gelu".  n_in defaults to
+    h_in's width, else n_dyad * bi."""
     D, bo, bi = w1.shape
     M, n_out = dz.shape
-    n_in = D * bi
+    _width(n_out, D, bo, "n_out")
+    n_in = _width(n_in if n_in is not None or h_in is None else h_in.shape[1], D, bi, "n_in")
     dx = torch.empty((M, n_in), dtype=dz.dtype, device=dz.device)
     _check(dyad_backward_dx(_variant(variant), n_in, n_out, D, M, _dtype(dz, w1, w2, h_in),
                             _ptr(dz), _ptr(w1), _ptr(w2), _act(act_in), _ptr(h_in), _ptr(dx),
@@ -177,7 +193,7 @@ def backward_dw(dz, x, n_dyad, variant="IT", want_db=True, workspace=None):
     n_in = x.shape[1]
     D = n_dyad
     dt = _dtype(dz, x)
-    shp = (D, n_out // D if n_out % D == 0 else 0, n_in // D if n_in % D == 0 else 0)
+    shp = (D, -(-n_out // D), -(-n_in // D))   # widths zero-padded up to n_dyad blocks
     dw1 = torch.empty(shp, dtype=dz.dtype, device=dz.device)
     dw2 = torch.empty(shp, dtype=dz.dtype, device=dz.device)
     db = torch.empty((n_out,), dtype=dz.dtype, device=dz.device) if want_db else None

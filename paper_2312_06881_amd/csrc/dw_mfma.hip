@@ -40,6 +40,7 @@ constexpr Cand kCands[] = {
 
 bool choose(const DwPass &p, DwPlan &pl) {
     if (p.dtype != kBF16 || p.M <= 0) return false;
+    if (p.n_in != p.D * p.bi || p.n_out != p.D * p.bo) return false;  // zero-padded widths
     if (p.D != 1 && p.D != 2 && p.D != 4 && p.D != 8 && p.D != 16) return false;
     // 32-bit buffer offsets within one stage (32 token rows of the wider operand)
     if ((int64_t)kStageK * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;

@@ -13,6 +13,9 @@ using dyad::GemmPass;
 constexpr int64_t kMaxDim = (int64_t)1 << 31;   // any single width or token count
 constexpr int64_t kMaxElems = (int64_t)1 << 40; // any single tensor, in elements
 
+// Per-block size; a width that D does not divide is zero-padded up to D blocks.
+int64_t block(int64_t n, int64_t D) { return (n + D - 1) / D; }
+
 bool aligned16(const void *p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
 
 int check_sizes(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t M, int dtype) {
@@ -21,7 +24,7 @@ int check_sizes(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t M, 
     if (n_in <= 0 || n_out <= 0 || D <= 0 || M < 0) return DYAD_ERR_INVALID_ARG;
     if (n_in >= kMaxDim || n_out >= kMaxDim || M >= kMaxDim) return DYAD_ERR_INVALID_ARG;
     if (M * n_in >= kMaxElems || M * n_out >= kMaxElems) return DYAD_ERR_INVALID_ARG;
-    if (n_in % D || n_out % D) return DYAD_ERR_SHAPE;
+    if (D >= kMaxDim || D * block(n_in, D) * block(n_out, D) >= kMaxElems) return DYAD_ERR_INVALID_ARG;
     return DYAD_OK;
 }
 
@@ -55,7 +58,7 @@ int dyad_forward(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dy
         return DYAD_ERR_ALIGN;
     if (M == 0) return DYAD_OK;
     GemmPass p{};
-    p.M = M; p.Kin = n_in; p.Nout = n_out; p.D = n_dyad; p.bk = n_in / n_dyad; p.bn = n_out / n_dyad;
+    p.M = M; p.Kin = n_in; p.Nout = n_out; p.D = n_dyad; p.bk = block(n_in, n_dyad); p.bn = block(n_out, n_dyad);
     p.in_t = in_transposed(variant); p.out_t = out_transposed(variant); p.w_t = false;
     p.dtype = dtype;
     p.epilogue = act == DYAD_ACT_GELU ? dyad::kEpiBiasGelu : dyad::kEpiBias;
@@ -76,7 +79,7 @@ int dyad_backward_dx(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t 
         return DYAD_ERR_ALIGN;
     if (M == 0) return DYAD_OK;
     GemmPass p{};
-    p.M = M; p.Kin = n_out; p.Nout = n_in; p.D = n_dyad; p.bk = n_out / n_dyad; p.bn = n_in / n_dyad;
+    p.M = M; p.Kin = n_out; p.Nout = n_in; p.D = n_dyad; p.bk = block(n_out, n_dyad); p.bn = block(n_in, n_dyad);
     p.in_t = out_transposed(variant); p.out_t = in_transposed(variant); p.w_t = true;
     p.dtype = dtype;
     p.epilogue = act_in == DYAD_ACT_GELU ? dyad::kEpiGeluGrad : dyad::kEpiBias;
@@ -86,7 +89,7 @@ int dyad_backward_dx(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t 
 
 static DwPass make_dw(int variant, int64_t n_in, int64_t n_out, int64_t D, int64_t M, int dtype) {
     DwPass p{};
-    p.M = M; p.n_in = n_in; p.n_out = n_out; p.D = D; p.bi = n_in / D; p.bo = n_out / D;
+    p.M = M; p.n_in = n_in; p.n_out = n_out; p.D = D; p.bi = block(n_in, D); p.bo = block(n_out, D);
     p.in_t = in_transposed(variant); p.out_t = out_transposed(variant); p.dtype = dtype;
     return p;
 }
@@ -119,7 +122,7 @@ const char *dyad_strerror(int status) {
     switch (status) {
     case DYAD_OK: return "ok";
     case DYAD_ERR_INVALID_ARG: return "invalid argument (enum, size or NULL pointer)";
-    case DYAD_ERR_SHAPE: return "n_in and n_out must be divisible by n_dyad";
+    case DYAD_ERR_SHAPE: return "unsupported shape";
     case DYAD_ERR_ALIGN: return "pointer not 16-byte aligned";
     case DYAD_ERR_DTYPE: return "unsupported dtype";
     case DYAD_ERR_WORKSPACE: return "dW workspace missing or too small";

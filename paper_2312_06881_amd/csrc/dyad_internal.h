@@ -17,10 +17,13 @@ enum Epilogue {
 };
 
 // One pass of the Dyad grouped GEMM, written for both the forward pass and the
-// input gradient.  With D groups, per-group input width bk = Kin/D and output
-// width bn = Nout/D, for every token m and output feature f:
+// input gradient.  With D groups, per-group input width bk = ceil(Kin/D) and
+// output width bn = ceil(Nout/D), for every token m and output feature f < Nout:
 //   out[m][f] = sum over the stored entries (c, i, j, k) whose output column is f
+//               and whose input column is < Kin
 //               of Wc(i, j, k) * in[m][input column of (c, i, k)]
+// (widths that D does not divide are zero-padded: the missing input columns
+// read as zero and the output columns past Nout are never written).
 // where
 //   output column: comp 1 -> i*bn + j;  comp 2 -> out_t ? j*D + i : i*bn + j
 //   input column:  comp 1 -> i*bk + k;  comp 2 -> in_t  ? k*D + i : i*bk + k
@@ -40,6 +43,8 @@ struct GemmPass {
 // Weight/bias gradient of one layer (forward-variant flags in_t/out_t):
 //   dWc[i][j][k] = sum_m dZ[m][row_c(i, j)] * X[m][col_c(i, k)],  db[f] = sum_m dZ[m][f]
 // row_c = comp 1 or !out_t ? i*bo + j : j*D + i;  col_c = comp 1 or !in_t ? i*bi + k : k*D + i.
+// bi = ceil(n_in/D), bo = ceil(n_out/D); an entry with row_c >= n_out or
+// col_c >= n_in touches only zero-padding and gets a zero gradient.
 struct DwPass {
     int64_t M, n_in, n_out, D, bi, bo;
     bool in_t, out_t;
@@ -55,7 +60,8 @@ hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t s);
 hipError_t launch_simt_dw(const DwPass &p, hipStream_t s);
 
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
-// when the pass's shape has no matching tile configuration.
+// when the pass's shape has no matching tile configuration (zero-padded
+// widths included).
 hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t s);
 
 // MFMA weight gradient (bf16): split over tokens, fixed-order reduction of the

@@ -7,6 +7,8 @@ namespace dyad {
 
 hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t s) {
     if (p.dtype != kBF16) return hipErrorNotSupported;
+    // zero-padded widths (Kin or Nout not D times the block size) stay on the SIMT path
+    if (p.Kin != p.D * p.bk || p.Nout != p.D * p.bn) return hipErrorNotSupported;
     if (!p.w_t) {
         if (p.in_t && !p.out_t) return launch_mfma_fwd_it(p, s);
         if (!p.in_t && p.out_t) return launch_mfma_fwd_ot(p, s);

@@ -1,6 +1,7 @@
 // SIMT kernels: one thread per output element, fp32 accumulation in natural
-// k order.  They accept any shape (any n_dyad, any block sizes) and both
-// dtypes; the fp32 path and every shape the MFMA kernels do not cover use them.
+// k order.  They accept any shape (any n_dyad, any block sizes, widths that
+// n_dyad does not divide) and both dtypes; the fp32 path and every shape the
+// MFMA kernels do not cover use them.
 #include "dyad_device.h"
 #include "dyad_internal.h"
 
@@ -18,16 +19,19 @@ __global__ void __launch_bounds__(256) simt_gemm_kernel(GemmPass p) {
          e += (int64_t)gridDim.x * blockDim.x) {
         const int64_t m = e / p.Nout, f = e % p.Nout;
         const T *x = in + m * p.Kin;
-        // comp 1: block-diagonal, i = f / bn, j = f % bn
+        // comp 1: block-diagonal, i = f / bn, j = f % bn; input columns past Kin
+        // are zero-padding and are skipped
         int64_t i = f / p.bn, j = f % p.bn;
         float acc = 0.f;
-        for (int64_t k = 0; k < p.bk; ++k) {
+        const int64_t k1 = min(p.bk, p.Kin - i * p.bk);
+        for (int64_t k = 0; k < k1; ++k) {
             int64_t w = p.w_t ? (i * p.bk + k) * p.bn + j : (i * p.bn + j) * p.bk + k;
             acc += load_f32(W1, w) * load_f32(x, i * p.bk + k);
         }
         // comp 2: output column f came from (i, j) by the inverse of its output map
         if (p.out_t) { i = f % p.D; j = f / p.D; }
-        for (int64_t k = 0; k < p.bk; ++k) {
+        const int64_t k2 = min(p.bk, p.in_t ? (p.Kin - i + p.D - 1) / p.D : p.Kin - i * p.bk);
+        for (int64_t k = 0; k < k2; ++k) {
             int64_t w = p.w_t ? (i * p.bk + k) * p.bn + j : (i * p.bn + j) * p.bk + k;
             int64_t c = p.in_t ? k * p.D + i : i * p.bk + k;
             acc += load_f32(W2, w) * load_f32(x, c);
@@ -57,8 +61,10 @@ __global__ void __launch_bounds__(256) simt_dw_kernel(DwPass p) {
         const int64_t r = e % per, i = r / (p.bo * p.bi), j = (r / p.bi) % p.bo, k = r % p.bi;
         const int64_t row = (comp == 1 || !p.out_t) ? i * p.bo + j : j * p.D + i;
         const int64_t col = (comp == 1 || !p.in_t) ? i * p.bi + k : k * p.D + i;
+        // an entry in a zero-padded row or column gets a zero gradient
+        const int64_t M = (row < p.n_out && col < p.n_in) ? p.M : 0;
         float acc = 0.f;
-        for (int64_t m = 0; m < p.M; ++m) acc += load_f32(dZ, m * p.n_out + row) * load_f32(X, m * p.n_in + col);
+        for (int64_t m = 0; m < M; ++m) acc += load_f32(dZ, m * p.n_out + row) * load_f32(X, m * p.n_in + col);
         store_f32(static_cast<T *>(comp == 1 ? p.dW1 : p.dW2), r, acc);
     }
 }

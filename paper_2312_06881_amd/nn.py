@@ -3,16 +3,18 @@
 * ``DyadLinear``: one Dyad layer, y = W x + b with W = BlockDiag(W1) +
   BlockTrans(W2) in the IT / OT / DT form (paper Sec. 3, Eqs. 1-16), a
   replacement for ``torch.nn.Linear``.
-* ``DyadFF``: the feed-forward block fc1 -> GELU -> fc2 with both layers Dyad.
-  The forward writes GELU(fc1) and stashes fc1's pre-activation in the same
+* ``DyadFF``: the feed-forward block fc1 -> GELU -> fc2 with both layers Dyad,
+  each with its own variant if wanted (a heterogeneous mix, Sec. 5).  The
+  forward writes GELU(fc1) and stashes fc1's pre-activation in the same
   epilogue; the backward applies GELU' inside fc2's input-gradient epilogue,
   so the activation gradient is never a separate pass.
 
 Autograd runs every pass through the C-ABI (forward, input gradient, weight and
 bias gradient); there is no torch fallback and CPU tensors are rejected.
 Leading input dimensions are flattened into the token dimension.  Weights
-are stored as [n_dyad, out/n_dyad, in/n_dyad] tensors, W1 the BlockDiag and W2
-the BlockTrans component.
+are stored as [n_dyad, ceil(out/n_dyad), ceil(in/n_dyad)] tensors, W1 the
+BlockDiag and W2 the BlockTrans component; widths that n_dyad does not divide
+are zero-padded (appendix, caveat on rectangular W).
 """
 from __future__ import annotations
 
@@ -31,29 +33,32 @@ def _tokens(x: torch.Tensor) -> torch.Tensor:
 
 class _DyadLinearFn(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, w1, w2, bias, variant):
+    def forward(ctx, x, w1, w2, bias, variant, n_out):
         ctx.variant = variant
         ctx.has_bias = bias is not None
         ctx.save_for_backward(x, w1, w2)
-        return forward(x, w1, w2, bias, variant)
+        return forward(x, w1, w2, bias, variant, n_out=n_out)
 
     @staticmethod
     def backward(ctx, dy):
         x, w1, w2 = ctx.saved_tensors
         dy = dy.contiguous()
-        dx = backward_dx(dy, w1, w2, ctx.variant) if ctx.needs_input_grad[0] else None
+        dx = None
+        if ctx.needs_input_grad[0]:
+            dx = backward_dx(dy, w1, w2, ctx.variant, n_in=x.shape[1])
         dw1 = dw2 = db = None
         if any(ctx.needs_input_grad[1:4]):
             dw1, dw2, db = backward_dw(dy, x, w1.shape[0], ctx.variant, want_db=ctx.has_bias)
-        return dx, dw1, dw2, db, None
+        return dx, dw1, dw2, db, None, None
 
 
 class _DyadFFFn(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x, w1a, w2a, ba, w1b, w2b, bb, variant):
-        a, h = forward(x, w1a, w2a, ba, variant, act="gelu", stash_h=True)
-        y = forward(a, w1b, w2b, bb, variant)
-        ctx.variant = variant
+    def forward(ctx, x, w1a, w2a, ba, w1b, w2b, bb, variants, ffn, d_out):
+        va, vb = variants
+        a, h = forward(x, w1a, w2a, ba, va, act="gelu", stash_h=True, n_out=ffn)
+        y = forward(a, w1b, w2b, bb, vb, n_out=d_out)
+        ctx.variants = variants
         ctx.bias = (ba is not None, bb is not None)
         ctx.save_for_backward(x, h, a, w1a, w2a, w1b, w2b)
         return y
@@ -61,48 +66,64 @@ class _DyadFFFn(torch.autograd.Function):
     @staticmethod
     def backward(ctx, dy):
         x, h, a, w1a, w2a, w1b, w2b = ctx.saved_tensors
-        v = ctx.variant
+        va, vb = ctx.variants
         dy = dy.contiguous()
         # fc2: input gradient times GELU'(fc1 pre-activation), then its weights
-        dz1 = backward_dx(dy, w1b, w2b, v, act_in="gelu", h_in=h)
-        dw1b, dw2b, dbb = backward_dw(dy, a, w1b.shape[0], v, want_db=ctx.bias[1])
+        dz1 = backward_dx(dy, w1b, w2b, vb, act_in="gelu", h_in=h)
+        dw1b, dw2b, dbb = backward_dw(dy, a, w1b.shape[0], vb, want_db=ctx.bias[1])
         # fc1
-        dx = backward_dx(dz1, w1a, w2a, v) if ctx.needs_input_grad[0] else None
-        dw1a, dw2a, dba = backward_dw(dz1, x, w1a.shape[0], v, want_db=ctx.bias[0])
-        return dx, dw1a, dw2a, dba, dw1b, dw2b, dbb, None
+        dx = backward_dx(dz1, w1a, w2a, va, n_in=x.shape[1]) if ctx.needs_input_grad[0] else None
+        dw1a, dw2a, dba = backward_dw(dz1, x, w1a.shape[0], va, want_db=ctx.bias[0])
+        return dx, dw1a, dw2a, dba, dw1b, dw2b, dbb, None, None, None
 
 
-def dyad_linear(x, w1, w2, bias=None, variant="IT"):
-    """Functional form of ``DyadLinear``: x [..., n_in] -> [..., n_out]."""
+def _variant_pair(variant):
+    pair = (variant, variant) if isinstance(variant, str) else tuple(variant)
+    if len(pair) != 2 or any(v not in ("IT", "OT", "DT") for v in pair):
+        raise ValueError("variant is one of IT, OT, DT, or an (fc1, fc2) pair of them")
+    return pair
+
+
+def dyad_linear(x, w1, w2, bias=None, variant="IT", out_features=None):
+    """Functional form of ``DyadLinear``: x [..., n_in] -> [..., n_out], where n_out is
+    out_features, else bias's length, else n_dyad * bo."""
     D, bo, _ = w1.shape
-    y = _DyadLinearFn.apply(_tokens(x), w1, w2, bias, variant)
-    return y.reshape(*x.shape[:-1], D * bo)
+    if out_features is None:
+        out_features = bias.shape[0] if bias is not None else D * bo
+    y = _DyadLinearFn.apply(_tokens(x), w1, w2, bias, variant, out_features)
+    return y.reshape(*x.shape[:-1], out_features)
 
 
-def dyad_ff(x, fc1, fc2, variant="IT"):
-    """Functional form of ``DyadFF``; fc1 / fc2 are (W1, W2, bias) triples."""
-    D, bo, _ = fc2[0].shape
-    y = _DyadFFFn.apply(_tokens(x), *fc1, *fc2, variant)
-    return y.reshape(*x.shape[:-1], D * bo)
+def dyad_ff(x, fc1, fc2, variant="IT", ffn=None):
+    """Functional form of ``DyadFF``; fc1 / fc2 are (W1, W2, bias) triples; variant is one
+    variant or an (fc1, fc2) pair; ffn is the hidden width (default n_dyad * fc1's bo).
+    The output width is x's, as the block is d -> ffn -> d."""
+    d = x.shape[-1]
+    if ffn is None:
+        ffn = fc1[0].shape[0] * fc1[0].shape[1]
+    y = _DyadFFFn.apply(_tokens(x), *fc1, *fc2, _variant_pair(variant), ffn, d)
+    return y.reshape(*x.shape[:-1], d)
 
 
 class DyadLinear(torch.nn.Module):
     """Dyad replacement for ``torch.nn.Linear(in_features, out_features)``.
 
-    ``n_dyad`` must divide both widths.  Initialisation (a convenience, not part
-    of the method): uniform in +-1/sqrt(2 * in_features / n_dyad), the fan-in of
-    one output feature (two components of in_features / n_dyad inputs each).
+    A width that ``n_dyad`` does not divide is zero-padded up to the next multiple
+    (appendix, caveat on rectangular W); such layers run on the library's general
+    kernels rather than the matrix-core ones.  Initialisation (a convenience, not
+    part of the method): uniform in +-1/sqrt(2 * in_features / n_dyad), the
+    fan-in of one output feature (two components of in_features / n_dyad inputs each).
     """
 
     def __init__(self, in_features, out_features, n_dyad, variant="IT", bias=True, device=None,
                  dtype=torch.bfloat16):
         super().__init__()
-        if in_features % n_dyad or out_features % n_dyad:
-            raise ValueError("n_dyad must divide in_features and out_features")
+        if min(in_features, out_features, n_dyad) <= 0:
+            raise ValueError("widths and n_dyad must be positive")
         if variant not in ("IT", "OT", "DT"):
             raise ValueError("variant is one of IT, OT, DT")
         self.in_features, self.out_features, self.n_dyad, self.variant = in_features, out_features, n_dyad, variant
-        shape = (n_dyad, out_features // n_dyad, in_features // n_dyad)
+        shape = (n_dyad, -(-out_features // n_dyad), -(-in_features // n_dyad))
         kw = {"device": device, "dtype": dtype}
         self.w1 = torch.nn.Parameter(torch.empty(shape, **kw))
         self.w2 = torch.nn.Parameter(torch.empty(shape, **kw))
@@ -117,7 +138,7 @@ class DyadLinear(torch.nn.Module):
                     p.uniform_(-bound, bound)
 
     def forward(self, x):
-        return dyad_linear(x, self.w1, self.w2, self.bias, self.variant)
+        return dyad_linear(x, self.w1, self.w2, self.bias, self.variant, self.out_features)
 
     def extra_repr(self):
         return (f"in_features={self.in_features}, out_features={self.out_features}, "
@@ -125,14 +146,20 @@ class DyadLinear(torch.nn.Module):
 
 
 class DyadFF(torch.nn.Module):
-    """Feed-forward block fc1 (d -> ffn) -> GELU -> fc2 (ffn -> d), both Dyad layers."""
+    """Feed-forward block fc1 (d -> ffn) -> GELU -> fc2 (ffn -> d), both Dyad layers.
+
+    ``variant`` is one of IT / OT / DT for both layers, or an (fc1, fc2) pair for a
+    heterogeneous mix; ``n_dyad`` likewise may be one value or a pair."""
 
     def __init__(self, d, ffn, n_dyad, variant="IT", bias=True, device=None, dtype=torch.bfloat16):
         super().__init__()
-        self.fc1 = DyadLinear(d, ffn, n_dyad, variant, bias, device, dtype)
-        self.fc2 = DyadLinear(ffn, d, n_dyad, variant, bias, device, dtype)
-        self.variant = variant
+        va, vb = _variant_pair(variant)
+        da, db = (n_dyad, n_dyad) if isinstance(n_dyad, int) else tuple(n_dyad)
+        self.fc1 = DyadLinear(d, ffn, da, va, bias, device, dtype)
+        self.fc2 = DyadLinear(ffn, d, db, vb, bias, device, dtype)
+        self.variant = (va, vb)
+        self.ffn = ffn
 
     def forward(self, x):
         return dyad_ff(x, (self.fc1.w1, self.fc1.w2, self.fc1.bias),
-                       (self.fc2.w1, self.fc2.w2, self.fc2.bias), self.variant)
+                       (self.fc2.w1, self.fc2.w2, self.fc2.bias), self.variant, self.ffn)

@@ -58,8 +58,12 @@ FAKE = 1 << 20  # a 16-byte-aligned non-NULL address; never dereferenced by reje
     (dict(n_out=-4), -1),
     (dict(n_dyad=0), -1),
     (dict(M=-1), -1),
-    (dict(n_in=66), -2),
-    (dict(n_out=258), -2),
+    (dict(n_dyad=1 << 31), -1),
+    (dict(n_in=1 << 30, n_out=1 << 30, n_dyad=2), -1),   # 2^59 weight entries
+    # widths that n_dyad does not divide are accepted (zero-padded): the next
+    # check in line reports instead
+    (dict(n_in=66, X=FAKE + 8), -3),
+    (dict(n_out=258, Y=None), -1),
     (dict(M=1 << 31), -1),
     (dict(W1=None), -1),
     (dict(X=None), -1),
@@ -84,7 +88,7 @@ def test_forward_empty_batch_is_a_noop():
     (dict(act_in=2), -1),
     (dict(dZ=None), -1),
     (dict(dX=FAKE + 4), -3),
-    (dict(n_in=63), -2),
+    (dict(n_in=63, dX=FAKE + 4), -3),
 ])
 def test_backward_dx_rejects(args, code):
     a = dict(variant=1, n_in=64, n_out=256, n_dyad=4, M=8, dtype=1, dZ=FAKE, W1=FAKE, W2=FAKE,
@@ -102,6 +106,7 @@ def test_backward_dw_rejects_and_workspace_size():
         assert dy.dyad_backward_dw(**dict(a, workspace=FAKE, workspace_bytes=need - 1)) == -5
     assert dy.dyad_backward_dw(**dict(a, dW2=None)) == -1
     assert dy.dyad_backward_dw(**dict(a, X=FAKE + 1)) == -3
-    assert dy.dyad_backward_dw(**dict(a, n_dyad=5)) == -2
+    assert dy.dyad_backward_dw(**dict(a, n_dyad=5, X=FAKE + 1)) == -3   # padded widths pass the shape check
+    # padded widths run on the general kernels, which need no workspace
     assert dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 1) == 0
     assert dy.dyad_dw_workspace_bytes(9, 768, 3072, 4, 16384, 1) == 0

@@ -103,3 +103,63 @@ def test_linear_no_bias_and_frozen_weights():
     assert_close(mod(x).detach(), ry, "bf16", "y")
     assert_close(x.grad, rdx, "bf16", "dx")
     assert mod.w1.grad is None and mod.w2.grad is None
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+def test_linear_padded_autograd(variant):
+    """A layer whose widths n_dyad does not divide (zero-padded blocks), fp32 and bf16."""
+    n_in, n_out, D, M = 250, 100, 3, 37
+    for dtype, tdt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+        banner("linear_padded", variant, dtype)
+        L = layer_inputs(n_in, n_out, D, M, dtype)
+        mod = DyadLinear(n_in, n_out, D, variant, device=DEV, dtype=tdt)
+        assert mod.w1.shape == L.W1.shape
+        load_layer(mod, L)
+        x = L.X.to(DEV).requires_grad_(True)
+        y = mod(x)
+        assert y.shape == (M, n_out)
+        y.backward(L.dZ.to(DEV))
+        torch.cuda.synchronize()
+        ry = oracle.forward(variant, n_in, n_out, D, L.f64("X"), L.f64("W1"), L.f64("W2"), L.f64("bias"))
+        rdx = oracle.backward_dx(variant, n_in, n_out, D, L.f64("dZ"), L.f64("W1"), L.f64("W2"))
+        rw1, rw2, rb = oracle.backward_dw(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"))
+        assert_close(y, ry, dtype, "y")
+        assert_close(x.grad, rdx, dtype, "dx")
+        assert_close(mod.w1.grad, rw1, dtype, "dW1")
+        assert_close(mod.w2.grad, rw2, dtype, "dW2")
+        assert_close(mod.bias.grad, rb, dtype, "db")
+
+
+@pytest.mark.parametrize("variants,dyads,ffn", [(("IT", "OT"), (4, 4), 1024), (("DT", "IT"), (8, 2), 1024),
+                                               (("OT", "DT"), (4, 3), 1000)])
+def test_ff_variant_mix(variants, dyads, ffn):
+    """DyadFF with a different variant (and n_dyad) per layer; the last case pads fc2's blocks."""
+    d, M = 256, 130
+    va, vb = variants
+    Da, Db = dyads
+    banner("ff_mix", variants, dyads, ffn)
+    L1 = layer_inputs(d, ffn, Da, M, "bf16")
+    L2 = layer_inputs(ffn, d, Db, M, "bf16", seed_offset=100)
+    ff = DyadFF(d, ffn, dyads, variants, device=DEV)
+    load_layer(ff.fc1, L1)
+    load_layer(ff.fc2, L2)
+    x = L1.X.to(DEV).requires_grad_(True)
+    y = ff(x)
+    y.backward(L2.dZ.to(DEV))
+    torch.cuda.synchronize()
+    X = L1.f64("X")
+    ra1, rh1 = oracle.forward(va, d, ffn, Da, X, L1.f64("W1"), L1.f64("W2"), L1.f64("bias"),
+                              act=oracle.ACT_GELU, want_h=True)
+    ry = oracle.forward(vb, ffn, d, Db, ra1, L2.f64("W1"), L2.f64("W2"), L2.f64("bias"))
+    rdh = oracle.backward_dx(vb, ffn, d, Db, L2.f64("dZ"), L2.f64("W1"), L2.f64("W2"),
+                             act_in=oracle.ACT_GELU, H_in=rh1)
+    r21, r22, rb2 = oracle.backward_dw(vb, ffn, d, Db, L2.f64("dZ"), ra1)
+    rdx = oracle.backward_dx(va, d, ffn, Da, rdh, L1.f64("W1"), L1.f64("W2"))
+    r11, r12, rb1 = oracle.backward_dw(va, d, ffn, Da, rdh, X)
+    for got, ref, what in ((y, ry, "y"), (x.grad, rdx, "dx"), (ff.fc2.w1.grad, r21, "fc2.dW1"),
+                           (ff.fc2.w2.grad, r22, "fc2.dW2"), (ff.fc2.bias.grad, rb2, "fc2.db"),
+                           (ff.fc1.w1.grad, r11, "fc1.dW1"), (ff.fc1.w2.grad, r12, "fc1.dW2"),
+                           (ff.fc1.bias.grad, rb1, "fc1.db")):
+        g = to64(got)
+        err = float(np.abs(g - ref).max() / np.abs(ref).max())
+        assert err <= 2e-2, (what, err)

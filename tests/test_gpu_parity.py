@@ -211,10 +211,72 @@ def test_ff_chain(variant):
                            (dx, rdx, "dx"), (g11, r11, "dW11"), (g12, r12, "dW12"),
                            (gb1, rb1, "db1")):
         # each layer rounds its output to bf16 before the next consumes it, so the
-        # chain is held to the spec bar only, not the per-layer elementwise bound
+        # chain is held to the max-norm bar only, not the per-layer elementwise bound
         g = to64(got)
         err = float(np.abs(g - ref).max() / np.abs(ref).max())
         assert err <= 2e-2, (what, err)
+
+
+# ---- widths that n_dyad does not divide: zero-padded layers -------------------
+
+PADDED = [  # (n_in, n_out, n_dyad, M)
+    (6, 7, 2, 5),          # the appendix's 7 x 6 weight at n_dyad 2
+    (250, 510, 4, 77),
+    (768, 3072, 5, 96),    # OPT-125m fc1 widths at n_dyad 5: blocks of 154 and 615
+    (3072, 768, 5, 40),
+    (100, 36, 8, 33),      # blocks of 13 and 5
+    (5, 9, 8, 17),         # n_dyad above n_in: three groups see only padding
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", PADDED, ids=case_id)
+def test_padded_all_passes(shape, variant, dtype):
+    """Forward (GELU, H stash), input gradient (GELU'), weight and bias gradients of a
+    zero-padded layer; outputs are written through the C-ABI into buffers with a guard
+    tail that must stay untouched (no write lands past n_out or n_in)."""
+    n_in, n_out, D, M = shape
+    banner("padded", shape, variant, dtype)
+    L = layer_inputs(n_in, n_out, D, M, dtype)
+    tdt = L.X.dtype
+    code = dy.BF16 if dtype == "bf16" else dy.F32
+    v = dy.VARIANTS[variant]
+    x, w1, w2, b, dz, hin = (gpu(t) for t in (L.X, L.W1, L.W2, L.bias, L.dZ, L.H_in))
+    guard = 64
+    sentinel = -1536.0   # exact in bf16
+
+    def guarded(n):
+        return torch.full((n + guard,), sentinel, dtype=tdt, device=DEV)
+
+    y, h, dx = guarded(M * n_out), guarded(M * n_out), guarded(M * n_in)
+    bo, bi = w1.shape[1], w1.shape[2]
+    dw1, dw2, db = guarded(D * bo * bi), guarded(D * bo * bi), guarded(n_out)
+    s = torch.cuda.current_stream().cuda_stream
+    assert dy.dyad_forward(v, n_in, n_out, D, M, code, x.data_ptr(), w1.data_ptr(), w2.data_ptr(),
+                           b.data_ptr(), dy.ACT_GELU, y.data_ptr(), h.data_ptr(), s) == 0
+    assert dy.dyad_backward_dx(v, n_in, n_out, D, M, code, dz.data_ptr(), w1.data_ptr(),
+                               w2.data_ptr(), dy.ACT_GELU, hin.data_ptr(), dx.data_ptr(), s) == 0
+    assert dy.dyad_dw_workspace_bytes(v, n_in, n_out, D, M, code) == 0
+    assert dy.dyad_backward_dw(v, n_in, n_out, D, M, code, dz.data_ptr(), x.data_ptr(),
+                               dw1.data_ptr(), dw2.data_ptr(), db.data_ptr(), None, 0, s) == 0
+    torch.cuda.synchronize()
+    for t in (y, h, dx, dw1, dw2, db):
+        assert bool((t[-guard:] == sentinel).all()), "write past the end of an output"
+    ry, rh = oracle.forward(variant, n_in, n_out, D, L.f64("X"), L.f64("W1"), L.f64("W2"),
+                            L.f64("bias"), act=oracle.ACT_GELU, want_h=True)
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, L.f64("dZ"), L.f64("W1"), L.f64("W2"),
+                             act_in=oracle.ACT_GELU, H_in=L.f64("H_in"))
+    r1, r2, rb = oracle.backward_dw(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"))
+    assert_close(y[:-guard].view(M, n_out), ry, dtype, "Y")
+    assert_close(h[:-guard].view(M, n_out), rh, dtype, "H")
+    assert_close(dx[:-guard].view(M, n_in), rdx, dtype, "dX")
+    assert_close(dw1[:-guard].view(D, bo, bi), r1, dtype, "dW1")
+    assert_close(dw2[:-guard].view(D, bo, bi), r2, dtype, "dW2")
+    assert_close(db[:-guard], rb, dtype, "db")
+    # entries that touch only padding get exactly zero
+    assert bool((dw1[:-guard].view(D, bo, bi)[torch.from_numpy(r1 == 0).to(DEV)] == 0).all())
+    assert bool((dw2[:-guard].view(D, bo, bi)[torch.from_numpy(r2 == 0).to(DEV)] == 0).all())
 
 
 # ---- full-size named workloads, sampled ---------------------------------------

@@ -22,9 +22,23 @@ def test_parameter_shapes_and_init_bound():
 
 def test_invalid_arguments():
     with pytest.raises(ValueError):
-        DyadLinear(64, 250, 4)
+        DyadLinear(64, 0, 4)
     with pytest.raises(ValueError):
         DyadLinear(64, 256, 4, "XT")
+    with pytest.raises(ValueError):
+        DyadFF(64, 256, 4, ("IT", "OT", "DT"))
+    with pytest.raises(ValueError):
+        DyadFF(64, 256, 4, ("IT", "XT"))
+
+
+def test_padded_widths_and_variant_mix():
+    """Widths n_dyad does not divide get zero-padded blocks; DyadFF takes per-layer variants."""
+    mod = DyadLinear(250, 7, 4, "OT")
+    assert mod.w1.shape == mod.w2.shape == (4, 2, 63)
+    assert mod.bias.shape == (7,)
+    ff = DyadFF(768, 3072, (5, 4), ("IT", "DT"))
+    assert ff.fc1.w1.shape == (5, 615, 154) and ff.fc2.w1.shape == (4, 192, 768)
+    assert ff.variant == ("IT", "DT") and ff.fc1.variant == "IT" and ff.fc2.variant == "DT"
 
 
 def test_cpu_tensors_refused():

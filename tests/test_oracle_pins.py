@@ -335,3 +335,134 @@ def test_gelu_against_normal_cdf():
     assert oracle.gelu_grad(0.0) == 0.5
     assert oracle.gelu(1.0) == pytest.approx(0.8413447460685429, rel=1e-15)  # Phi(1)
     assert math.isclose(oracle.gelu_grad(30.0), 1.0)
+
+
+# ---- widths that n_dyad does not divide: zero-padding (appendix, caveat on rectangular W) ----
+
+PADDED = [  # (n_in, n_out, D) with D dividing at most one width
+    (6, 7, 2),        # the appendix's 7 x 6 weight: one zero row makes n_dyad 2 possible
+    (10, 13, 4),
+    (30, 17, 3),
+    (5, 9, 8),        # bi = 1, bo = 2: most entries touch padding
+    (12, 10, 4),      # n_in divisible, n_out not
+]
+
+
+def padded_blocks(n_in, n_out, D):
+    return -(-n_in // D), -(-n_out // D)
+
+
+def padded_dense(variant, n_in, n_out, D, W1, W2):
+    """Dense weight of the zero-padded layer: the divisible layer of widths D*bi -> D*bo
+    (assembled through block_diag and P), restricted to its first n_out rows and n_in columns."""
+    bi, bo = padded_blocks(n_in, n_out, D)
+    return dense_weight(variant, D * bi, D * bo, D, W1, W2)[:n_out, :n_in]
+
+
+def padded_case(n_in, n_out, D, M, seed):
+    rng = np.random.default_rng(seed)
+    bi, bo = padded_blocks(n_in, n_out, D)
+    return (rng.standard_normal((M, n_in)), rng.standard_normal((D, bo, bi)),
+            rng.standard_normal((D, bo, bi)), rng.standard_normal(n_out))
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+@pytest.mark.parametrize("shape", PADDED)
+def test_padded_forward_is_cropped_dense(variant, shape):
+    n_in, n_out, D = shape
+    X, W1, W2, b = padded_case(n_in, n_out, D, 5, 81)
+    Y = oracle.forward(variant, n_in, n_out, D, X, W1, W2, b)
+    W = padded_dense(variant, n_in, n_out, D, W1, W2)
+    np.testing.assert_allclose(Y, X @ W.T + b, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+@pytest.mark.parametrize("shape", PADDED)
+def test_padded_layer_is_divisible_layer_on_zero_padded_input(variant, shape):
+    """The caveat's recipe taken literally: append zero input features, run the layer whose
+    widths n_dyad divides, keep the first n_out outputs.  GELU and the H stash follow."""
+    n_in, n_out, D = shape
+    bi, bo = padded_blocks(n_in, n_out, D)
+    X, W1, W2, b = padded_case(n_in, n_out, D, 4, 82)
+    Xp = np.zeros((4, D * bi))
+    Xp[:, :n_in] = X
+    bp = np.concatenate([b, np.random.default_rng(83).standard_normal(D * bo - n_out)])
+    Yp, Hp = oracle.forward(variant, D * bi, D * bo, D, Xp, W1, W2, bp, act=ACT_GELU, want_h=True)
+    Y, H = oracle.forward(variant, n_in, n_out, D, X, W1, W2, b, act=ACT_GELU, want_h=True)
+    np.testing.assert_array_equal(Y, Yp[:, :n_out])
+    np.testing.assert_array_equal(H, Hp[:, :n_out])
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+@pytest.mark.parametrize("shape", PADDED)
+def test_padded_backward_matches_dense_gradient(variant, shape):
+    """dX = dZ W over the cropped dense W; dW_c is the padded layer's dense gradient (dZ and X
+    with zero columns appended) gathered through block_diag and P, so entries that touch
+    padding get exactly zero."""
+    n_in, n_out, D = shape
+    bi, bo = padded_blocks(n_in, n_out, D)
+    M = 6
+    X, W1, W2, _ = padded_case(n_in, n_out, D, M, 84)
+    dZ = np.random.default_rng(85).standard_normal((M, n_out))
+    W = padded_dense(variant, n_in, n_out, D, W1, W2)
+    np.testing.assert_allclose(oracle.backward_dx(variant, n_in, n_out, D, dZ, W1, W2), dZ @ W,
+                               rtol=1e-12, atol=1e-12)
+    Xp = np.zeros((M, D * bi))
+    Xp[:, :n_in] = X
+    dZp = np.zeros((M, D * bo))
+    dZp[:, :n_out] = dZ
+    G = dZp.T @ Xp
+    P_in, P_out = perm_eq5(D, bi), perm_eq5(D, bo)
+    G2 = {"IT": G @ P_in.T, "OT": P_out @ G, "DT": P_out @ G @ P_in.T}[variant]
+
+    def blocks(A):
+        return np.stack([A[i * bo:(i + 1) * bo, i * bi:(i + 1) * bi] for i in range(D)])
+
+    dW1, dW2, db = oracle.backward_dw(variant, n_in, n_out, D, dZ, X)
+    np.testing.assert_allclose(dW1, blocks(G), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dW2, blocks(G2), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, dZ.sum(0), rtol=1e-12, atol=1e-12)
+    comp = np.repeat([1, 2], D * bo * bi)
+    i, j, k = (a.ravel() for a in np.meshgrid(np.arange(D), np.arange(bo), np.arange(bi), indexing="ij"))
+    i, j, k = np.tile(i, 2), np.tile(j, 2), np.tile(k, 2)
+    got = oracle.backward_dw_entries(variant, n_in, n_out, D, dZ, X, comp, i, j, k)
+    np.testing.assert_allclose(got, np.concatenate([dW1.ravel(), dW2.ravel()]), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
+def test_padded_backward_finite_differences(variant):
+    n_in, n_out, D = 6, 7, 2
+    M = 2
+    X, W1, W2, b = padded_case(n_in, n_out, D, M, 86)
+    G = np.random.default_rng(87).standard_normal((M, n_out))
+    dX = oracle.backward_dx(variant, n_in, n_out, D, G, W1, W2)
+    dW1, dW2, db = oracle.backward_dw(variant, n_in, n_out, D, G, X)
+    eps = 1e-6
+    L = lambda X_, W1_, W2_, b_: flat_loss(variant, n_in, n_out, D, X_, W1_, W2_, b_, G, ACT_NONE)  # noqa
+    for arr, grad, idx in ((X, dX, 0), (W1, dW1, 1), (W2, dW2, 2), (b, db, 3)):
+        num = np.zeros_like(arr)
+        for pos in np.ndindex(arr.shape):
+            args_p = [X.copy(), W1.copy(), W2.copy(), b.copy()]
+            args_m = [X.copy(), W1.copy(), W2.copy(), b.copy()]
+            args_p[idx][pos] += eps
+            args_m[idx][pos] -= eps
+            num[pos] = (L(*args_p) - L(*args_m)) / (2 * eps)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7)
+
+
+def test_appendix_7x6_example_live_entries():
+    """The appendix's 7 x 6 weight with n_dyad 2: one zero row pads it to 8 x 6, blocks 4 x 3.
+    Of the 2 * 8 * 6 / 2 = 48 stored entries, the 3 + 3 that sit in the padded row (W1 block 1,
+    row 3 and its BlockTrans partner) do not reach the 7 x 6 weight; the other 42 each do."""
+    n_in, n_out, D = 6, 7, 2
+    for v in ("IT", "OT", "DT"):
+        live = 0
+        for c in (1, 2):
+            for idx in np.ndindex(D, 4, 3):
+                W1 = np.zeros((D, 4, 3))
+                W2 = np.zeros((D, 4, 3))
+                (W1 if c == 1 else W2)[idx] = 1.0
+                Wd = oracle.forward(v, n_in, n_out, D, np.eye(n_in), W1, W2).T   # column e = W e
+                live += int(np.count_nonzero(Wd) == 1)
+                assert np.count_nonzero(Wd) <= 1
+        assert live == 42, v

@@ -58,7 +58,7 @@ class LayerInputs:
 def layer_inputs(n_in: int, n_out: int, n_dyad: int, M: int, dtype: str = "bf16",
                  bias: str = "normal", seed_offset: int = 0) -> LayerInputs:
     """Inputs for one layer; ``bias`` is "normal", "zero" or "none"."""
-    bo, bi = n_out // n_dyad, n_in // n_dyad
+    bo, bi = -(-n_out // n_dyad), -(-n_in // n_dyad)   # widths zero-padded up to n_dyad blocks
     X = draw("X", (M, n_in), 1.0, dtype, seed_offset)
     W1 = draw("W1", (n_dyad, bo, bi), W_STD, dtype, seed_offset)
     W2 = draw("W2", (n_dyad, bo, bi), W_STD, dtype, seed_offset)
