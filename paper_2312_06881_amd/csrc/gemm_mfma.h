@@ -81,7 +81,7 @@ struct GemmCfg {
     static_assert(kLds <= 160 * 1024, "LDS budget");
 };
 
-template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int OCC>
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int OCC, int PF = 1>
 __global__ void __launch_bounds__(64 * WGM * WGN, OCC)
 dyad_gemm_mfma(GemmArgs a) {
     using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
@@ -159,12 +159,16 @@ dyad_gemm_mfma(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < C::kSubN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    uint4 ra[C::kRC][C::kVecPerRC2];
-    uint4 rb[W_T ? C::kRBT : C::kRB][W_T ? 8 : 1];
+    // PF register sets of staged operands: the loads of a stage are issued PF
+    // stages before its operands are written to LDS
+    uint4 ras[PF][C::kRC][C::kVecPerRC2];
+    uint4 rbs[PF][W_T ? C::kRBT : C::kRB][W_T ? 8 : 1];
 
-    // ---- global -> registers for stage s of component 1 or 2
-    auto fetch = [&](auto comp, int s) {
+    // ---- global -> registers (set `set`) for stage s of component 1 or 2
+    auto fetch = [&](auto comp, int s, auto set) {
         constexpr bool C2 = decltype(comp)::value;
+        auto &ra = ras[decltype(set)::value];
+        auto &rb = rbs[decltype(set)::value];
         const uint32_t kk = (uint32_t)((C2 ? s - ks : s) * kStageK);
 #pragma unroll
         for (int q = 0; q < C::kRC; ++q) {
@@ -195,9 +199,11 @@ dyad_gemm_mfma(GemmArgs a) {
         }
     };
 
-    // ---- registers -> LDS stage buffer
-    auto stash = [&](auto comp, uint16_t *buf) {
+    // ---- registers (set `set`) -> LDS stage buffer
+    auto stash = [&](auto comp, uint16_t *buf, auto set) {
         constexpr bool C2 = decltype(comp)::value;
+        auto &ra = ras[decltype(set)::value];
+        auto &rb = rbs[decltype(set)::value];
         uint16_t *bufB = buf + C::kStageA;
 #pragma unroll
         for (int q = 0; q < C::kRC; ++q) {
@@ -284,47 +290,88 @@ dyad_gemm_mfma(GemmArgs a) {
     // (pointer arithmetic on the LDS array keeps these LDS accesses; an array of
     // pointers would turn them into flat ones)
     auto buf = [&](int idx) -> uint16_t * { return lds + (idx & 1) * C::kStageElems; };
-    if (ks == 1) {
-        fetch(Comp1{}, 0);
-        stash(Comp1{}, buf(0));
-        fetch(Comp2{}, 1);
+    using Set0 = std::integral_constant<int, 0>;
+    using Set1 = std::integral_constant<int, 1>;
+    if constexpr (PF == 2) {
+        // Loads run two stages ahead, and the two components alternate: stage
+        // 2j is the BlockDiag stage j, stage 2j+1 the BlockTrans stage j.  A
+        // stage's kind, register set and LDS buffer all follow its parity, so
+        // every iteration is straight-line code and the wait before each stash
+        // leaves the next stage's loads in flight.  Iteration t stashes stage
+        // t+1, fetches stage t+3 into the register set that stash freed, and
+        // multiplies stage t.
+        // (launched only with at least two stages per component, so that no
+        // branch precedes the loop: a join there would make the compiler wait
+        // for every load in flight)
+        fetch(Comp1{}, 0, Set0{});
+        fetch(Comp2{}, ks, Set1{});
+        stash(Comp1{}, buf(0), Set0{});
+        fetch(Comp1{}, 1, Set0{});
         __syncthreads();
-        stash(Comp2{}, buf(1));
+        int j = 0;
+        for (; j + 2 < ks; ++j) {
+            stash(Comp2{}, buf(1), Set1{});          // BlockTrans stage j
+            fetch(Comp2{}, ks + j + 1, Set1{});
+            compute(Comp1{}, buf(0));                 // BlockDiag stage j
+            __syncthreads();
+            stash(Comp1{}, buf(0), Set0{});           // BlockDiag stage j+1
+            fetch(Comp1{}, j + 2, Set0{});
+            compute(Comp2{}, buf(1));                 // BlockTrans stage j
+            __syncthreads();
+        }
+        stash(Comp2{}, buf(1), Set1{});               // j = ks - 2
+        fetch(Comp2{}, ks + j + 1, Set1{});
+        compute(Comp1{}, buf(0));
+        __syncthreads();
+        stash(Comp1{}, buf(0), Set0{});
+        compute(Comp2{}, buf(1));
+        __syncthreads();
+        stash(Comp2{}, buf(1), Set1{});               // j = ks - 1
+        compute(Comp1{}, buf(0));
+        __syncthreads();
+        compute(Comp2{}, buf(1));
+        __syncthreads();
+    } else if (ks == 1) {
+        fetch(Comp1{}, 0, Set0{});
+        stash(Comp1{}, buf(0), Set0{});
+        fetch(Comp2{}, 1, Set0{});
+        __syncthreads();
+        stash(Comp2{}, buf(1), Set0{});
         compute(Comp1{}, buf(0));
         __syncthreads();
         compute(Comp2{}, buf(1));
         __syncthreads();
     } else {
-        fetch(Comp1{}, 0);
-        stash(Comp1{}, buf(0));
-        fetch(Comp1{}, 1);
+        fetch(Comp1{}, 0, Set0{});
+        stash(Comp1{}, buf(0), Set0{});
+        fetch(Comp1{}, 1, Set0{});
         __syncthreads();
         int s = 0;
         for (; s + 2 < ks; ++s) {
-            stash(Comp1{}, buf(s + 1));
-            fetch(Comp1{}, s + 2);
+            stash(Comp1{}, buf(s + 1), Set0{});
+            fetch(Comp1{}, s + 2, Set0{});
             compute(Comp1{}, buf(s));
             __syncthreads();
         }
         // s = ks - 2: the stage after next is the first BlockTrans stage
-        stash(Comp1{}, buf(s + 1));
-        fetch(Comp2{}, s + 2);
+        stash(Comp1{}, buf(s + 1), Set0{});
+        fetch(Comp2{}, s + 2, Set0{});
         compute(Comp1{}, buf(s));
         __syncthreads();
         ++s;
         // s = ks - 1
-        stash(Comp2{}, buf(s + 1));
-        fetch(Comp2{}, s + 2);
+        stash(Comp2{}, buf(s + 1), Set0{});
+        fetch(Comp2{}, s + 2, Set0{});
         compute(Comp1{}, buf(s));
         __syncthreads();
         ++s;
         for (; s + 2 < S; ++s) {
-            stash(Comp2{}, buf(s + 1));
-            fetch(Comp2{}, s + 2);
+            stash(Comp2{}, buf(s + 1), Set0{});
+            fetch(Comp2{}, s + 2, Set0{});
             compute(Comp2{}, buf(s));
             __syncthreads();
         }
-        stash(Comp2{}, buf(s + 1));
+        stash(Comp2{}, buf(s + 1), Set0{});
         compute(Comp2{}, buf(s));
         __syncthreads();
         ++s;

@@ -70,14 +70,34 @@ __device__ __forceinline__ uint4 deinterleave(const uint4 (&v)[D]) {
     return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
-// Residue r, a value uniform across the workgroup, of the span: one branch per
-// residue, each a compile-time shuffle.
-template <int D, int R = 0>
+// Residue r (0 <= r < D, uniform across the workgroup, known only at run
+// time) of the span, without branches: element e = 2wD + r sits in vector
+// e / 8 (a compile-time base, plus one when r carries it over, which only
+// n_dyad 16 can do), word (e % 8) / 2 and half r % 2, so each output word is
+// a select or two and one v_perm_b32.  Branch-free code keeps a pipelined main
+// loop straight-line, which the compiler needs to wait on exact load counts.
+template <int D>
+__device__ __forceinline__ uint32_t span_word(const uint4 (&v)[D], int c, int r) {
+    // element c + r, c a multiple of D fixed at compile time after unrolling;
+    // below n_dyad 16 the vector is c / 8 for every r < D
+    const int base = c >> 3;
+    uint4 x = v[base];
+    if constexpr (D > 8)
+        if (((c & 7) + r) >= 8) x = v[base + 1 < D ? base + 1 : base];
+    return word_of(x, ((c + r) & 7) >> 1);
+}
+
+template <int D>
 __device__ __forceinline__ uint4 deinterleave_uniform(const uint4 (&v)[D], int r) {
-    if constexpr (R + 1 < D) {
-        if (r != R) return deinterleave_uniform<D, R + 1>(v, r);
+    uint32_t o[4];
+    const uint32_t sel = perm_sel((r & 1) * 2, 4 + ((r + D) & 1) * 2);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const uint32_t a = span_word<D>(v, 2 * w * D, r);
+        const uint32_t b = span_word<D>(v, (2 * w + 1) * D, r);
+        o[w] = __builtin_amdgcn_perm(b, a, sel);
     }
-    return deinterleave<D, R>(v);
+    return make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // Every residue of the span into its own LDS slab (slab R at dst + R * slab).

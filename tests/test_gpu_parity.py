@@ -217,6 +217,22 @@ def test_ff_chain(variant):
         assert err <= 2e-2, (what, err)
 
 
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", [(256, 768, 4, 16461), (384, 768, 4, 16400), (768, 768, 4, 16384)],
+                         ids=case_id)
+def test_forward_bias_large_batch_full(shape, variant):
+    """Forward with a bias epilogue at batches that fill the GPU with 256 x 192 tiles (the
+    path that keeps two stages of loads in flight), every output checked: two, three and
+    twelve stages per component, and a ragged last token tile."""
+    n_in, n_out, D, M = shape
+    banner("forward_large", shape, variant)
+    L = layer_inputs(n_in, n_out, D, M, "bf16")
+    y = dy.forward(gpu(L.X), gpu(L.W1), gpu(L.W2), gpu(L.bias), variant=variant)
+    torch.cuda.synchronize()
+    ry = oracle.forward(variant, n_in, n_out, D, L.f64("X"), L.f64("W1"), L.f64("W2"), L.f64("bias"))
+    assert_close(y, ry, "bf16", "Y")
+
+
 # ---- widths that n_dyad does not divide: zero-padded layers -------------------
 
 PADDED = [  # (n_in, n_out, n_dyad, M)
