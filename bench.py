@@ -52,7 +52,7 @@ def parse():
 
 def workload(name):
     import workloads as W
-    table = {w.name: w for w in [W.OPT125M, W.OPT350M, W.TINY, *W.SWEEP, *W.WIDE]}
+    table = {w.name: w for w in [W.OPT125M, W.OPT350M, W.TINY, *W.SWEEP, *W.WIDE, *W.PADDED]}
     if name not in table:
         raise SystemExit(f"unknown workload {name}; choose from {sorted(table)}")
     return table[name]

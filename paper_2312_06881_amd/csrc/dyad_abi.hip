@@ -35,11 +35,17 @@ int launch_status(hipError_t e) { return e == hipSuccess ? DYAD_OK : DYAD_ERR_LA
 
 int run_gemm(const GemmPass &p, hipStream_t s) {
     hipError_t e = dyad::launch_mfma_gemm(p, s);
+    if (e == hipErrorNotSupported) e = dyad::launch_general_mfma_gemm(p, s);
     if (e == hipErrorNotSupported) e = dyad::launch_simt_gemm(p, s);
     return launch_status(e);
 }
 
-size_t dw_workspace(const DwPass &p) { return dyad::mfma_dw_workspace(p); }
+// Workspace of the weight-gradient path the call will take: the MFMA kernels
+// for shapes they cover, else the general matrix-core kernel.
+size_t dw_workspace(const DwPass &p) {
+    const size_t w = dyad::mfma_dw_workspace(p);
+    return w ? w : dyad::general_dw_workspace(p);
+}
 
 }  // namespace
 
@@ -113,7 +119,8 @@ int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t 
     size_t need = dw_workspace(p);
     if (need > 0 && (!workspace || workspace_bytes < need)) return DYAD_ERR_WORKSPACE;
     p.dZ = dZ; p.X = X; p.dW1 = dW1; p.dW2 = dW2; p.db = dbias; p.ws = workspace; p.ws_bytes = workspace_bytes;
-    hipError_t e = need > 0 ? dyad::launch_mfma_dw(p, stream) : hipErrorNotSupported;
+    hipError_t e = dyad::mfma_dw_workspace(p) > 0 ? dyad::launch_mfma_dw(p, stream) : hipErrorNotSupported;
+    if (e == hipErrorNotSupported && M > 0) e = dyad::launch_general_mfma_dw(p, stream);
     if (e == hipErrorNotSupported) e = dyad::launch_simt_dw(p, stream);
     return launch_status(e);
 }

@@ -55,9 +55,22 @@ struct DwPass {
     size_t ws_bytes;
 };
 
-// SIMT kernels: any shape, any D, both dtypes.
+// General kernels: any shape, any D, both dtypes (vector ALU, tiled).
 hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t s);
 hipError_t launch_simt_dw(const DwPass &p, hipStream_t s);
+// db alone (fixed-order token sums), as the general weight-gradient paths use it.
+hipError_t launch_db(const DwPass &p, hipStream_t s);
+
+// General weight gradient on the matrix cores (bf16, any shape), token splits
+// summed in order through the workspace: general_dw_workspace() bytes (0 when
+// one split suffices or the path does not apply).
+size_t general_dw_workspace(const DwPass &p);
+hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s);
+
+// General grouped GEMM on the matrix cores (bf16, any shape): operands
+// gathered element by element.  hipErrorNotSupported for fp32 or offsets past
+// 32 bits.
+hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s);
 
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
 // when the pass's shape has no matching tile configuration (zero-padded

@@ -1,0 +1,417 @@
+// Matrix-core forms of the general kernels (bf16): any n_dyad, any block
+// sizes, zero-padded widths.
+//
+// Grouped GEMM (forward, input gradient).  It keeps the class decomposition of the vector
+// kernel in kernels_simt.hip -- the output columns of class (g1, g2) all read
+// input columns g1*bk + k (BlockDiag) and c2(g2, k) (BlockTrans), so a tile of
+// 128 tokens x 128 columns of one class is a plain GEMM with K = 2*bk -- and
+// multiplies on v_mfma_f32_16x16x32_bf16.  Operands are gathered element by
+// element with 2-byte buffer loads (no alignment or divisibility is assumed;
+// reads past a width or past the batch return zero), packed in pairs into the
+// swizzled LDS rows the MFMA fragments read, double-buffered with one barrier
+// per 32-deep chunk.  Every thread issues the same loads every chunk (invalid
+// elements point past the buffer), so the compiler's wait counts stay exact.
+//
+// Weight gradient.  dWc[g][j][k] = sum_m dZ[m][row_c(g, j)] X[m][col_c(g, k)]
+// as 128 x 128 tiles of (component, group) products over K = tokens, the
+// tokens split across workgroups when the tiles alone would not fill the GPU;
+// fp32 partials per split go to the workspace and are added in split order.
+#include <type_traits>
+
+#include "dyad_internal.h"
+#include "mfma_common.h"
+
+namespace dyad {
+namespace {
+
+constexpr int kGM = 128, kGN = 128;   // tokens x class columns per tile, 4 waves of 64 x 64
+constexpr int kPairs = 8;             // element pairs per thread and operand per chunk
+
+struct GClass {
+    int64_t g1, g2, first, step, count;
+};
+
+__device__ GClass gclass(const GemmPass &p, int64_t cls) {
+    GClass c;
+    const int64_t D = p.D;
+    if (!p.out_t) {
+        c.g1 = c.g2 = cls;
+        c.first = cls * p.bn;
+        c.step = 1;
+        const int64_t end = min((cls + 1) * p.bn, p.Nout);
+        c.count = end > c.first ? end - c.first : 0;
+    } else {
+        c.g1 = cls / D;
+        c.g2 = cls % D;
+        const int64_t lo = c.g1 * p.bn, hi = min((c.g1 + 1) * p.bn, p.Nout);
+        c.first = lo + ((c.g2 - lo % D) % D + D) % D;   // first f >= lo with f % D == g2
+        c.step = D;
+        c.count = hi > c.first ? (hi - c.first + D - 1) / D : 0;
+    }
+    return c;
+}
+
+__device__ __forceinline__ uint32_t ld2(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, 0, 0);
+}
+
+__global__ void __launch_bounds__(256, 2) general_mfma_kernel(GemmPass p, int col_tiles, int row_tiles) {
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kGM * kStageK];   // [buffer][A, B]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x;
+    const int rt = b % row_tiles, ct = (b / row_tiles) % col_tiles, cls = b / (row_tiles * col_tiles);
+    const GClass cc = gclass(p, cls);
+    const int t0 = ct * kGN;
+    if (t0 >= cc.count) return;                        // uniform: the whole block leaves
+    const int64_t m0 = (int64_t)rt * kGM;
+    const int64_t rows_left = p.M - m0;
+    const int bk = (int)p.bk, bn = (int)p.bn, D = (int)p.D, Kin = (int)p.Kin;
+    const int nk = 2 * bk, chunks = (nk + kStageK - 1) / kStageK;
+
+    const uint16_t *in = static_cast<const uint16_t *>(p.in);
+    const uint32_t a_bytes = (uint32_t)((rows_left < kGM ? rows_left : kGM) * p.Kin * 2);
+    const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(in + m0 * p.Kin, a_bytes);
+    const uint32_t w_bytes = (uint32_t)(p.D * p.bn * p.bk * 2);
+    const __amdgpu_buffer_rsrc_t rW1 = buffer_rsrc(p.W1, w_bytes);
+    const __amdgpu_buffer_rsrc_t rW2 = buffer_rsrc(p.W2, w_bytes);
+
+    // Per-thread constants: pair q covers A row ar[q] at k pair akp[q], and
+    // class column bc[q] at k pair bkp[q].
+    int arow[kPairs], akp[kPairs], bkp[kPairs];
+    int bcol[kPairs];                  // class column within the tile
+    int bbase1[kPairs], bbase2[kPairs];   // weight element offsets at k = 0, -1 past the class
+#pragma unroll
+    for (int q = 0; q < kPairs; ++q) {
+        const int pi = tid + 256 * q;
+        akp[q] = pi & 15;
+        arow[q] = pi >> 4;
+        int ci;
+        if (p.w_t) { ci = pi & (kGN - 1); bkp[q] = pi >> 7; } else { bkp[q] = pi & 15; ci = pi >> 4; }
+        bcol[q] = ci;
+        const int64_t t = t0 + ci;
+        bbase1[q] = bbase2[q] = -1;
+        if (t < cc.count) {
+            const int64_t f = cc.first + t * cc.step;
+            const int64_t j1 = f - cc.g1 * p.bn, j2 = p.out_t ? f / p.D : j1;
+            bbase1[q] = (int)(p.w_t ? cc.g1 * p.bk * p.bn + j1 : (cc.g1 * p.bn + j1) * p.bk);
+            bbase2[q] = (int)(p.w_t ? cc.g2 * p.bk * p.bn + j2 : (cc.g2 * p.bn + j2) * p.bk);
+        }
+    }
+    const int a_col1 = (int)(cc.g1 * bk);
+    const int g2 = (int)cc.g2;
+
+    // element k of the concatenated K (BlockDiag, then BlockTrans)
+    auto a_off = [&](int q, int kq) -> uint32_t {
+        if (kq >= nk) return kNoLoad;
+        const int col = kq < bk ? a_col1 + kq : (p.in_t ? (kq - bk) * D + g2 : g2 * bk + (kq - bk));
+        if (col >= Kin) return kNoLoad;
+        return (uint32_t)(arow[q] * Kin + col) * 2u;
+    };
+    auto b_off = [&](int q, int kq) -> uint32_t {
+        if (kq >= nk || bbase1[q] < 0) return kNoLoad;
+        const bool c2 = kq >= bk;
+        const int k = c2 ? kq - bk : kq;
+        return (uint32_t)((c2 ? bbase2[q] : bbase1[q]) + (p.w_t ? k * bn : k)) * 2u;
+    };
+
+    uint32_t ra[kPairs][2], rb[kPairs][2];
+    // weights of a chunk: all BlockDiag, all BlockTrans, or (the one chunk that
+    // straddles k = bk) both, each element from its own tensor
+    auto fetch_b = [&](auto mode, int k0) {
+        constexpr int kMode = decltype(mode)::value;   // 1: W1 only, 2: W2 only, 3: both
+#pragma unroll
+        for (int q = 0; q < kPairs; ++q) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int kq = k0 + 2 * bkp[q] + h;
+                const uint32_t o = b_off(q, kq);
+                if constexpr (kMode == 1) rb[q][h] = ld2(rW1, o);
+                else if constexpr (kMode == 2) rb[q][h] = ld2(rW2, o);
+                else rb[q][h] = ld2(rW1, kq < bk ? o : kNoLoad) | ld2(rW2, kq < bk ? kNoLoad : o);
+            }
+        }
+    };
+    auto fetch = [&](int c) {
+        const int k0 = c * kStageK;
+#pragma unroll
+        for (int q = 0; q < kPairs; ++q) {
+            const int ka = k0 + 2 * akp[q];
+            ra[q][0] = ld2(rA, a_off(q, ka));
+            ra[q][1] = ld2(rA, a_off(q, ka + 1));
+        }
+        if (k0 + kStageK <= bk) fetch_b(std::integral_constant<int, 1>{}, k0);
+        else if (k0 >= bk) fetch_b(std::integral_constant<int, 2>{}, k0);
+        else fetch_b(std::integral_constant<int, 3>{}, k0);
+    };
+    auto stash = [&](int buf) {
+        uint16_t *A = lds[buf][0], *B = lds[buf][1];
+#pragma unroll
+        for (int q = 0; q < kPairs; ++q) {
+            *reinterpret_cast<uint32_t *>(A + lds_off(arow[q], akp[q] >> 2) + (akp[q] & 3) * 2) =
+                ra[q][0] | (ra[q][1] << 16);
+            *reinterpret_cast<uint32_t *>(B + lds_off(bcol[q], bkp[q] >> 2) + (bkp[q] & 3) * 2) =
+                rb[q][0] | (rb[q][1] << 16);
+        }
+    };
+
+    const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * 64;
+    const int lr = lane & 15, lc = lane >> 4;
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    fetch(0);
+    stash(0);
+    __syncthreads();
+    for (int c = 0; c < chunks; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < chunks) fetch(c + 1);
+        const uint16_t *A = lds[buf][0], *B = lds[buf][1];
+        bf16x8_t af[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t *>(A + lds_off(wm0 + 16 * i + lr, lc));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const bf16x8_t bf = *reinterpret_cast<const bf16x8_t *>(B + lds_off(wn0 + 16 * j + lr, lc));
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
+        }
+        if (c + 1 < chunks) stash(buf ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue straight from the accumulators: lane holds rows 4*(lane/16)+v,
+    // column lane%16 of each 16 x 16 block.
+    uint16_t *out = static_cast<uint16_t *>(p.out);
+    const uint16_t *bias = static_cast<const uint16_t *>(p.bias);
+    const uint16_t *h_in = static_cast<const uint16_t *>(p.h_in);
+    uint16_t *h_out = static_cast<uint16_t *>(p.h_out);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t t = t0 + wn0 + 16 * j + lr;
+        if (t >= cc.count) continue;
+        const int64_t f = cc.first + t * cc.step;
+        const float bv = (p.epilogue != kEpiGeluGrad && bias) ? bf16_to_f32(bias[f]) : 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t m = m0 + wm0 + 16 * i + 4 * lc + v;
+                if (m >= p.M) continue;
+                const int64_t e = m * p.Nout + f;
+                float x = acc[i][j][v];
+                if (p.epilogue == kEpiGeluGrad) {
+                    x *= gelu_grad(bf16_to_f32(h_in[e]));
+                } else {
+                    x += bv;
+                    if (p.epilogue == kEpiBiasGelu) {
+                        if (h_out) h_out[e] = f32_to_bf16(x);
+                        x = gelu(x);
+                    }
+                }
+                out[e] = f32_to_bf16(x);
+            }
+    }
+}
+
+// One split's tile of dW: rows j (dZ side), columns k (X side), K = tokens.
+__global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int jt_n, int kt_n, int splits,
+                                                                 int64_t tps, float *part) {
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kGM * kStageK];   // [buffer][dZ, X]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x;
+    const int kt = b % kt_n, jt = (b / kt_n) % jt_n, gc = (b / (kt_n * jt_n)) % (2 * (int)p.D);
+    const int split = b / (kt_n * jt_n * 2 * (int)p.D);
+    const int D = (int)p.D, comp = gc < D ? 1 : 2, g = gc % D;
+    const int bo = (int)p.bo, bi = (int)p.bi, n_out = (int)p.n_out, n_in = (int)p.n_in;
+    const int j0 = jt * kGM, k0 = kt * kGN;
+    const bool row_t = comp == 2 && p.out_t, col_t = comp == 2 && p.in_t;
+    const int64_t m_lo = (int64_t)split * tps;
+    const int64_t m_hi = min(m_lo + tps, p.M);
+    const int rows = (int)(m_hi > m_lo ? m_hi - m_lo : 0);
+    const int chunks = (rows + kStageK - 1) / kStageK;
+
+    const __amdgpu_buffer_rsrc_t rZ =
+        buffer_rsrc(static_cast<const uint16_t *>(p.dZ) + m_lo * p.n_out, (uint32_t)rows * (uint32_t)n_out * 2u);
+    const __amdgpu_buffer_rsrc_t rX =
+        buffer_rsrc(static_cast<const uint16_t *>(p.X) + m_lo * p.n_in, (uint32_t)rows * (uint32_t)n_in * 2u);
+
+    // pair q: entry column (j or k) pi % 128, token pair pi / 128
+    int zcol[kPairs], xcol[kPairs], mp[kPairs], ec[kPairs];
+#pragma unroll
+    for (int q = 0; q < kPairs; ++q) {
+        const int pi = tid + 256 * q;
+        ec[q] = pi & (kGM - 1);
+        mp[q] = pi >> 7;
+        const int j = j0 + ec[q], k = k0 + ec[q];
+        const int row = row_t ? j * D + g : g * bo + j;
+        const int col = col_t ? k * D + g : g * bi + k;
+        zcol[q] = (j < bo && row < n_out) ? row : -1;
+        xcol[q] = (k < bi && col < n_in) ? col : -1;
+    }
+    uint32_t rz[kPairs][2], rx[kPairs][2];
+    auto fetch = [&](int c) {
+#pragma unroll
+        for (int q = 0; q < kPairs; ++q)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t m = (uint32_t)(c * kStageK + 2 * mp[q] + h);
+                rz[q][h] = ld2(rZ, zcol[q] >= 0 ? (m * (uint32_t)n_out + (uint32_t)zcol[q]) * 2u : kNoLoad);
+                rx[q][h] = ld2(rX, xcol[q] >= 0 ? (m * (uint32_t)n_in + (uint32_t)xcol[q]) * 2u : kNoLoad);
+            }
+    };
+    auto stash = [&](int buf) {
+        uint16_t *Z = lds[buf][0], *Xs = lds[buf][1];
+#pragma unroll
+        for (int q = 0; q < kPairs; ++q) {
+            const int off = lds_off(ec[q], mp[q] >> 2) + (mp[q] & 3) * 2;
+            *reinterpret_cast<uint32_t *>(Z + off) = rz[q][0] | (rz[q][1] << 16);
+            *reinterpret_cast<uint32_t *>(Xs + off) = rx[q][0] | (rx[q][1] << 16);
+        }
+    };
+
+    const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * 64;
+    const int lr = lane & 15, lc = lane >> 4;
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (chunks > 0) {
+        fetch(0);
+        stash(0);
+    }
+    __syncthreads();
+    for (int c = 0; c < chunks; ++c) {
+        const int buf = c & 1;
+        if (c + 1 < chunks) fetch(c + 1);
+        const uint16_t *Z = lds[buf][0], *Xs = lds[buf][1];
+        bf16x8_t af[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t *>(Z + lds_off(wm0 + 16 * i + lr, lc));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const bf16x8_t bf = *reinterpret_cast<const bf16x8_t *>(Xs + lds_off(wn0 + 16 * j + lr, lc));
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
+        }
+        if (c + 1 < chunks) stash(buf ^ 1);
+        __syncthreads();
+    }
+
+    const int64_t per_comp = p.D * p.bo * p.bi;
+    uint16_t *dW = static_cast<uint16_t *>(comp == 1 ? p.dW1 : p.dW2);
+    float *dst = part ? part + (int64_t)split * 2 * per_comp + (comp - 1) * per_comp : nullptr;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = j0 + wm0 + 16 * i + 4 * lc + v;
+            if (j >= bo) continue;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int k = k0 + wn0 + 16 * jj + lr;
+                if (k >= bi) continue;
+                const int64_t e = ((int64_t)g * bo + j) * bi + k;
+                if (dst) dst[e] = acc[i][jj][v];
+                else dW[e] = f32_to_bf16(acc[i][jj][v]);
+            }
+        }
+}
+
+// dW = sum of the splits' partials, in split order.
+__global__ void __launch_bounds__(256) general_dw_reduce(const float *part, int splits, int64_t per_comp,
+                                                         uint16_t *dW1, uint16_t *dW2) {
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per_comp;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        float s = 0.f;
+        for (int q = 0; q < splits; ++q) s += part[(int64_t)q * 2 * per_comp + e];
+        uint16_t *out = e < per_comp ? dW1 + e : dW2 + (e - per_comp);
+        *out = f32_to_bf16(s);
+    }
+}
+
+struct GenDwPlan {
+    int jt, kt, splits;
+    int64_t tps;
+};
+
+bool gen_dw_plan(const DwPass &p, GenDwPlan &pl) {
+    if (p.dtype != kBF16) return false;
+    // 32-bit offsets within one split's token panel (checked with its rows below)
+    pl.jt = (int)((p.bo + kGM - 1) / kGM);
+    pl.kt = (int)((p.bi + kGN - 1) / kGN);
+    const int64_t tiles = 2 * p.D * pl.jt * pl.kt;
+    if (tiles >= ((int64_t)1 << 30)) return false;
+    // enough work items for two workgroups per CU, each at least 256 tokens deep
+    int64_t splits = tiles >= 512 ? 1 : (512 + tiles - 1) / tiles;
+    const int64_t max_splits = p.M / 256 > 0 ? p.M / 256 : 1;
+    if (splits > max_splits) splits = max_splits;
+    int64_t tps = (p.M + splits - 1) / splits;
+    tps = (tps + kStageK - 1) / kStageK * kStageK;
+    const int64_t wide = p.n_in > p.n_out ? p.n_in : p.n_out;
+    // 32-bit offsets: a split's rows plus one chunk of overrun stay below 2^31 bytes
+    if ((tps + kStageK) * wide * 2 >= ((int64_t)1 << 31)) {
+        tps = (((int64_t)1 << 31) / (wide * 2) - kStageK) / kStageK * kStageK;
+        if (tps < kStageK) return false;
+    }
+    pl.tps = tps > 0 ? tps : kStageK;
+    pl.splits = (int)((p.M + pl.tps - 1) / pl.tps);
+    if (pl.splits < 1) pl.splits = 1;
+    return tiles * pl.splits < ((int64_t)1 << 31);
+}
+
+}  // namespace
+
+hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s) {
+    if (p.dtype != kBF16) return hipErrorNotSupported;
+    if (p.M == 0) return hipSuccess;
+    // 32-bit buffer offsets: one token panel and one weight tensor must fit
+    if ((int64_t)kGM * p.Kin * 2 >= ((int64_t)1 << 31) || p.D * p.bn * p.bk * 2 >= ((int64_t)1 << 31))
+        return hipErrorNotSupported;
+    const int64_t classes = p.out_t ? p.D * p.D : p.D;
+    const int64_t per_class = p.out_t ? (p.bn + p.D - 1) / p.D + 1 : p.bn;
+    const int64_t col_tiles = (per_class + kGN - 1) / kGN;
+    const int64_t row_tiles = (p.M + kGM - 1) / kGM;
+    const int64_t blocks = classes * col_tiles * row_tiles;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    general_mfma_kernel<<<(unsigned)blocks, 256, 0, s>>>(p, (int)col_tiles, (int)row_tiles);
+    return hipGetLastError();
+}
+
+size_t general_dw_workspace(const DwPass &p) {
+    GenDwPlan pl;
+    if (!gen_dw_plan(p, pl) || pl.splits == 1) return 0;
+    return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi) * sizeof(float);
+}
+
+hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s) {
+    GenDwPlan pl;
+    if (!gen_dw_plan(p, pl)) return hipErrorNotSupported;
+    const int64_t per_comp = p.D * p.bo * p.bi;
+    float *part = nullptr;
+    if (pl.splits > 1) {
+        if (!p.ws || p.ws_bytes < (size_t)pl.splits * (size_t)(2 * per_comp) * sizeof(float))
+            return hipErrorInvalidValue;
+        part = static_cast<float *>(p.ws);
+    }
+    const int64_t blocks = (int64_t)pl.splits * 2 * p.D * pl.jt * pl.kt;
+    general_mfma_dw_kernel<<<(unsigned)blocks, 256, 0, s>>>(p, pl.jt, pl.kt, pl.splits, pl.tps, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (part) {
+        int64_t grid = (2 * per_comp + 255) / 256;
+        if (grid > 4096) grid = 4096;
+        general_dw_reduce<<<(unsigned)grid, 256, 0, s>>>(part, pl.splits, per_comp, static_cast<uint16_t *>(p.dW1),
+                                                         static_cast<uint16_t *>(p.dW2));
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return launch_db(p, s);
+}
+
+}  // namespace dyad

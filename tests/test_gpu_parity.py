@@ -242,6 +242,9 @@ PADDED = [  # (n_in, n_out, n_dyad, M)
     (3072, 768, 5, 40),
     (100, 36, 8, 33),      # blocks of 13 and 5
     (5, 9, 8, 17),         # n_dyad above n_in: three groups see only padding
+    (250, 510, 4, 1100),   # enough tokens to split the weight gradient (ragged last split)
+    (768, 3072, 5, 600),
+    (768, 3072, 3, 700),   # n_dyad 3 divides both widths; general kernels all the same
 ]
 
 
@@ -273,9 +276,13 @@ def test_padded_all_passes(shape, variant, dtype):
                            b.data_ptr(), dy.ACT_GELU, y.data_ptr(), h.data_ptr(), s) == 0
     assert dy.dyad_backward_dx(v, n_in, n_out, D, M, code, dz.data_ptr(), w1.data_ptr(),
                                w2.data_ptr(), dy.ACT_GELU, hin.data_ptr(), dx.data_ptr(), s) == 0
-    assert dy.dyad_dw_workspace_bytes(v, n_in, n_out, D, M, code) == 0
+    need = dy.dyad_dw_workspace_bytes(v, n_in, n_out, D, M, code)
+    ws = torch.empty((max(need, 16),), dtype=torch.uint8, device=DEV)
+    if need:   # a call without the workspace is refused before any launch
+        assert dy.dyad_backward_dw(v, n_in, n_out, D, M, code, dz.data_ptr(), x.data_ptr(), dw1.data_ptr(),
+                                   dw2.data_ptr(), db.data_ptr(), None, 0, s) == -5
     assert dy.dyad_backward_dw(v, n_in, n_out, D, M, code, dz.data_ptr(), x.data_ptr(),
-                               dw1.data_ptr(), dw2.data_ptr(), db.data_ptr(), None, 0, s) == 0
+                               dw1.data_ptr(), dw2.data_ptr(), db.data_ptr(), ws.data_ptr(), need, s) == 0
     torch.cuda.synchronize()
     for t in (y, h, dx, dw1, dw2, db):
         assert bool((t[-guard:] == sentinel).all()), "write past the end of an output"

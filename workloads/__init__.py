@@ -121,3 +121,10 @@ def wide(M: int) -> Workload:
 
 
 WIDE = [wide(M) for M in (16, 256, 32768)]
+
+
+# Widths that n_dyad does not divide (zero-padded blocks): OPT-125m's feed-forward
+# at n_dyad 3, 5 and 6 (blocks of 256/1024, 154/615 and 128/512)
+PADDED = [Workload(f"opt125m_ff_D{D}", d=768, ffn=3072, n_dyad=D, M=16384,
+                   note=f"OPT-125m FF at n_dyad={D}" + ("" if 768 % D == 0 else " (zero-padded blocks)"))
+          for D in (3, 5, 6)]
