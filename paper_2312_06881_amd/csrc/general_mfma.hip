@@ -31,7 +31,7 @@ struct GClass {
     int64_t g1, g2, first, step, count;
 };
 
-__device__ GClass gclass(const GemmPass &p, int64_t cls) {
+__device__ __forceinline__ GClass gclass(const GemmPass &p, int64_t cls) {
     GClass c;
     const int64_t D = p.D;
     if (!p.out_t) {
@@ -55,106 +55,137 @@ __device__ __forceinline__ uint32_t ld2(__amdgpu_buffer_rsrc_t r, uint32_t voff)
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)voff, 0, 0);
 }
 
+__device__ __forceinline__ uint32_t ld4(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, 0, 0);
+}
+
+// GM tokens x GN class columns per tile (4 waves of 64 x 64).  PAIRS: even
+// input width and block size, so every (k, k+1) pair of a contiguous operand
+// is one aligned 4-byte load.
+template <int GM, int GN, bool PAIRS, bool IN_T, bool W_T>
 __global__ void __launch_bounds__(256, 2) general_mfma_kernel(GemmPass p, int col_tiles, int row_tiles) {
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kGM * kStageK];   // [buffer][A, B]
+    constexpr int kPA = GM / 16, kPB = GN / 16;        // element pairs per thread per chunk
+    constexpr int kWGN = GN / 64;                      // waves along the columns
+    __shared__ __attribute__((aligned(16))) uint16_t ldsA[2][GM * kStageK];
+    __shared__ __attribute__((aligned(16))) uint16_t ldsB[2][GN * kStageK];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int b = blockIdx.x;
     const int rt = b % row_tiles, ct = (b / row_tiles) % col_tiles, cls = b / (row_tiles * col_tiles);
     const GClass cc = gclass(p, cls);
-    const int t0 = ct * kGN;
+    const int t0 = ct * GN;
     if (t0 >= cc.count) return;                        // uniform: the whole block leaves
-    const int64_t m0 = (int64_t)rt * kGM;
+    const int64_t m0 = (int64_t)rt * GM;
     const int64_t rows_left = p.M - m0;
     const int bk = (int)p.bk, bn = (int)p.bn, D = (int)p.D, Kin = (int)p.Kin;
     const int nk = 2 * bk, chunks = (nk + kStageK - 1) / kStageK;
 
     const uint16_t *in = static_cast<const uint16_t *>(p.in);
-    const uint32_t a_bytes = (uint32_t)((rows_left < kGM ? rows_left : kGM) * p.Kin * 2);
+    const uint32_t a_bytes = (uint32_t)((rows_left < GM ? rows_left : GM) * p.Kin * 2);
     const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(in + m0 * p.Kin, a_bytes);
     const uint32_t w_bytes = (uint32_t)(p.D * p.bn * p.bk * 2);
     const __amdgpu_buffer_rsrc_t rW1 = buffer_rsrc(p.W1, w_bytes);
     const __amdgpu_buffer_rsrc_t rW2 = buffer_rsrc(p.W2, w_bytes);
 
-    // Per-thread constants: pair q covers A row ar[q] at k pair akp[q], and
-    // class column bc[q] at k pair bkp[q].
-    int arow[kPairs], akp[kPairs], bkp[kPairs];
-    int bcol[kPairs];                  // class column within the tile
-    int bbase1[kPairs], bbase2[kPairs];   // weight element offsets at k = 0, -1 past the class
+    // Per-thread constants: A pair q is row arow[q], k pair akp[q]; B pair q is
+    // class column bcol[q], k pair bkp[q], weights at bbase{1,2}[q] + k (-1 past the class).
+    int arow[kPA], akp[kPA], bkp[kPB], bcol[kPB], bbase1[kPB], bbase2[kPB];
 #pragma unroll
-    for (int q = 0; q < kPairs; ++q) {
+    for (int q = 0; q < kPA; ++q) {
         const int pi = tid + 256 * q;
         akp[q] = pi & 15;
         arow[q] = pi >> 4;
+    }
+#pragma unroll
+    for (int q = 0; q < kPB; ++q) {
+        const int pi = tid + 256 * q;
         int ci;
-        if (p.w_t) { ci = pi & (kGN - 1); bkp[q] = pi >> 7; } else { bkp[q] = pi & 15; ci = pi >> 4; }
+        if constexpr (W_T) { ci = pi & (GN - 1); bkp[q] = pi / GN; } else { bkp[q] = pi & 15; ci = pi >> 4; }
         bcol[q] = ci;
         const int64_t t = t0 + ci;
         bbase1[q] = bbase2[q] = -1;
         if (t < cc.count) {
             const int64_t f = cc.first + t * cc.step;
             const int64_t j1 = f - cc.g1 * p.bn, j2 = p.out_t ? f / p.D : j1;
-            bbase1[q] = (int)(p.w_t ? cc.g1 * p.bk * p.bn + j1 : (cc.g1 * p.bn + j1) * p.bk);
-            bbase2[q] = (int)(p.w_t ? cc.g2 * p.bk * p.bn + j2 : (cc.g2 * p.bn + j2) * p.bk);
+            bbase1[q] = (int)(W_T ? cc.g1 * p.bk * p.bn + j1 : (cc.g1 * p.bn + j1) * p.bk);
+            bbase2[q] = (int)(W_T ? cc.g2 * p.bk * p.bn + j2 : (cc.g2 * p.bn + j2) * p.bk);
         }
     }
     const int a_col1 = (int)(cc.g1 * bk);
     const int g2 = (int)cc.g2;
 
-    // element k of the concatenated K (BlockDiag, then BlockTrans)
-    auto a_off = [&](int q, int kq) -> uint32_t {
+    // byte offset of element kq of the concatenated K (BlockDiag, then BlockTrans)
+    auto a_off = [&](int q, int kq) __attribute__((always_inline)) -> uint32_t {
         if (kq >= nk) return kNoLoad;
-        const int col = kq < bk ? a_col1 + kq : (p.in_t ? (kq - bk) * D + g2 : g2 * bk + (kq - bk));
+        const int col = kq < bk ? a_col1 + kq : (IN_T ? (kq - bk) * D + g2 : g2 * bk + (kq - bk));
         if (col >= Kin) return kNoLoad;
         return (uint32_t)(arow[q] * Kin + col) * 2u;
     };
-    auto b_off = [&](int q, int kq) -> uint32_t {
+    auto b_off = [&](int q, int kq) __attribute__((always_inline)) -> uint32_t {
         if (kq >= nk || bbase1[q] < 0) return kNoLoad;
         const bool c2 = kq >= bk;
         const int k = c2 ? kq - bk : kq;
-        return (uint32_t)((c2 ? bbase2[q] : bbase1[q]) + (p.w_t ? k * bn : k)) * 2u;
+        return (uint32_t)((c2 ? bbase2[q] : bbase1[q]) + (W_T ? k * bn : k)) * 2u;
     };
 
-    uint32_t ra[kPairs][2], rb[kPairs][2];
-    // weights of a chunk: all BlockDiag, all BlockTrans, or (the one chunk that
-    // straddles k = bk) both, each element from its own tensor
-    auto fetch_b = [&](auto mode, int k0) {
-        constexpr int kMode = decltype(mode)::value;   // 1: W1 only, 2: W2 only, 3: both
+    uint32_t ra[kPA], rb[kPB];                         // packed (k, k+1) pairs
+    // Chunk kinds (uniform): 1 all BlockDiag, 2 all BlockTrans, 3 the chunk
+    // that straddles k = bk, where every element picks its own form.
+    auto fetch_kind = [&](auto kind, int k0) __attribute__((always_inline)) {
+        constexpr int K = decltype(kind)::value;
 #pragma unroll
-        for (int q = 0; q < kPairs; ++q) {
+        for (int q = 0; q < kPA; ++q) {
+            const int kq = k0 + 2 * akp[q];
+            const uint32_t o0 = a_off(q, kq), o1 = a_off(q, kq + 1);
+            constexpr bool c1_pairs = PAIRS, c2_pairs = PAIRS && !IN_T;
+            if constexpr ((K == 1 && c1_pairs) || (K == 2 && c2_pairs) || (K == 3 && c1_pairs && c2_pairs)) {
+                ra[q] = ld4(rA, o0);
+            } else if constexpr (K == 3 && c1_pairs) {
+                // BlockDiag pairs contiguous, strided BlockTrans pairs element by element
+                const bool c2 = kq >= bk;
+                ra[q] = ld4(rA, c2 ? kNoLoad : o0) |
+                        (ld2(rA, c2 ? o0 : kNoLoad) | (ld2(rA, c2 ? o1 : kNoLoad) << 16));
+            } else {
+                ra[q] = ld2(rA, o0) | (ld2(rA, o1) << 16);
+            }
+        }
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int kq = k0 + 2 * bkp[q] + h;
-                const uint32_t o = b_off(q, kq);
-                if constexpr (kMode == 1) rb[q][h] = ld2(rW1, o);
-                else if constexpr (kMode == 2) rb[q][h] = ld2(rW2, o);
-                else rb[q][h] = ld2(rW1, kq < bk ? o : kNoLoad) | ld2(rW2, kq < bk ? kNoLoad : o);
+        for (int q = 0; q < kPB; ++q) {
+            const int kq = k0 + 2 * bkp[q];
+            const uint32_t o0 = b_off(q, kq), o1 = b_off(q, kq + 1);
+            if constexpr (PAIRS && !W_T) {
+                if constexpr (K == 1) rb[q] = ld4(rW1, o0);
+                else if constexpr (K == 2) rb[q] = ld4(rW2, o0);
+                else rb[q] = ld4(rW1, kq < bk ? o0 : kNoLoad) | ld4(rW2, kq < bk ? kNoLoad : o0);
+            } else {
+                uint32_t h[2];
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const uint32_t o = e ? o1 : o0;
+                    const int ke = kq + e;
+                    if constexpr (K == 1) h[e] = ld2(rW1, o);
+                    else if constexpr (K == 2) h[e] = ld2(rW2, o);
+                    else h[e] = ld2(rW1, ke < bk ? o : kNoLoad) | ld2(rW2, ke < bk ? kNoLoad : o);
+                }
+                rb[q] = h[0] | (h[1] << 16);
             }
         }
     };
-    auto fetch = [&](int c) {
+    auto fetch = [&](int c) __attribute__((always_inline)) {
         const int k0 = c * kStageK;
-#pragma unroll
-        for (int q = 0; q < kPairs; ++q) {
-            const int ka = k0 + 2 * akp[q];
-            ra[q][0] = ld2(rA, a_off(q, ka));
-            ra[q][1] = ld2(rA, a_off(q, ka + 1));
-        }
-        if (k0 + kStageK <= bk) fetch_b(std::integral_constant<int, 1>{}, k0);
-        else if (k0 >= bk) fetch_b(std::integral_constant<int, 2>{}, k0);
-        else fetch_b(std::integral_constant<int, 3>{}, k0);
+        if (k0 + kStageK <= bk) fetch_kind(std::integral_constant<int, 1>{}, k0);
+        else if (k0 >= bk) fetch_kind(std::integral_constant<int, 2>{}, k0);
+        else fetch_kind(std::integral_constant<int, 3>{}, k0);
     };
-    auto stash = [&](int buf) {
-        uint16_t *A = lds[buf][0], *B = lds[buf][1];
+    auto stash = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < kPairs; ++q) {
-            *reinterpret_cast<uint32_t *>(A + lds_off(arow[q], akp[q] >> 2) + (akp[q] & 3) * 2) =
-                ra[q][0] | (ra[q][1] << 16);
-            *reinterpret_cast<uint32_t *>(B + lds_off(bcol[q], bkp[q] >> 2) + (bkp[q] & 3) * 2) =
-                rb[q][0] | (rb[q][1] << 16);
-        }
+        for (int q = 0; q < kPA; ++q)
+            *reinterpret_cast<uint32_t *>(ldsA[buf] + lds_off(arow[q], akp[q] >> 2) + (akp[q] & 3) * 2) = ra[q];
+#pragma unroll
+        for (int q = 0; q < kPB; ++q)
+            *reinterpret_cast<uint32_t *>(ldsB[buf] + lds_off(bcol[q], bkp[q] >> 2) + (bkp[q] & 3) * 2) = rb[q];
     };
 
-    const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * 64;
+    const int wm0 = (wave / kWGN) * 64, wn0 = (wave % kWGN) * 64;
     const int lr = lane & 15, lc = lane >> 4;
     f32x4_t acc[4][4];
 #pragma unroll
@@ -168,7 +199,7 @@ __global__ void __launch_bounds__(256, 2) general_mfma_kernel(GemmPass p, int co
     for (int c = 0; c < chunks; ++c) {
         const int buf = c & 1;
         if (c + 1 < chunks) fetch(c + 1);
-        const uint16_t *A = lds[buf][0], *B = lds[buf][1];
+        const uint16_t *A = ldsA[buf], *B = ldsB[buf];
         bf16x8_t af[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t *>(A + lds_off(wm0 + 16 * i + lr, lc));
@@ -253,7 +284,7 @@ __global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int j
         xcol[q] = (k < bi && col < n_in) ? col : -1;
     }
     uint32_t rz[kPairs][2], rx[kPairs][2];
-    auto fetch = [&](int c) {
+    auto fetch = [&](int c) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < kPairs; ++q)
 #pragma unroll
@@ -263,7 +294,7 @@ __global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int j
                 rx[q][h] = ld2(rX, xcol[q] >= 0 ? (m * (uint32_t)n_in + (uint32_t)xcol[q]) * 2u : kNoLoad);
             }
     };
-    auto stash = [&](int buf) {
+    auto stash = [&](int buf) __attribute__((always_inline)) {
         uint16_t *Z = lds[buf][0], *Xs = lds[buf][1];
 #pragma unroll
         for (int q = 0; q < kPairs; ++q) {
@@ -365,22 +396,42 @@ bool gen_dw_plan(const DwPass &p, GenDwPlan &pl) {
     return tiles * pl.splits < ((int64_t)1 << 31);
 }
 
+template <int GM, int GN, bool PAIRS, bool IN_T, bool W_T>
+hipError_t launch_general_tile(const GemmPass &p, hipStream_t s) {
+    if ((int64_t)GM * p.Kin * 2 >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    const int64_t classes = p.out_t ? p.D * p.D : p.D;
+    const int64_t per_class = p.out_t ? (p.bn + p.D - 1) / p.D + 1 : p.bn;
+    const int64_t col_tiles = (per_class + GN - 1) / GN;
+    const int64_t row_tiles = (p.M + GM - 1) / GM;
+    const int64_t blocks = classes * col_tiles * row_tiles;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    general_mfma_kernel<GM, GN, PAIRS, IN_T, W_T><<<(unsigned)blocks, 256, 0, s>>>(p, (int)col_tiles, (int)row_tiles);
+    return hipGetLastError();
+}
+
+template <int GM, int GN>
+hipError_t launch_general_gn(const GemmPass &p, hipStream_t s) {
+    const bool pairs = p.Kin % 2 == 0 && p.bk % 2 == 0;
+#define DYAD_GEN(PR, IT, WT) \
+    if (pairs == PR && p.in_t == IT && p.w_t == WT) return launch_general_tile<GM, GN, PR, IT, WT>(p, s);
+    DYAD_GEN(true, false, false) DYAD_GEN(true, false, true) DYAD_GEN(true, true, false) DYAD_GEN(true, true, true)
+    DYAD_GEN(false, false, false) DYAD_GEN(false, false, true) DYAD_GEN(false, true, false) DYAD_GEN(false, true, true)
+#undef DYAD_GEN
+    return hipErrorNotSupported;
+}
+
 }  // namespace
 
 hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s) {
     if (p.dtype != kBF16) return hipErrorNotSupported;
     if (p.M == 0) return hipSuccess;
-    // 32-bit buffer offsets: one token panel and one weight tensor must fit
-    if ((int64_t)kGM * p.Kin * 2 >= ((int64_t)1 << 31) || p.D * p.bn * p.bk * 2 >= ((int64_t)1 << 31))
-        return hipErrorNotSupported;
-    const int64_t classes = p.out_t ? p.D * p.D : p.D;
-    const int64_t per_class = p.out_t ? (p.bn + p.D - 1) / p.D + 1 : p.bn;
-    const int64_t col_tiles = (per_class + kGN - 1) / kGN;
-    const int64_t row_tiles = (p.M + kGM - 1) / kGM;
-    const int64_t blocks = classes * col_tiles * row_tiles;
-    if (blocks >= ((int64_t)1 << 31)) return hipErrorNotSupported;
-    general_mfma_kernel<<<(unsigned)blocks, 256, 0, s>>>(p, (int)col_tiles, (int)row_tiles);
-    return hipGetLastError();
+    // 32-bit buffer offsets: one weight tensor must fit
+    if (p.D * p.bn * p.bk * 2 >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    // classes narrower than 128 columns (an output transpose leaves bn / D per
+    // class) take 256 x 64 tiles, which waste less of the tile
+    const int64_t per_class = p.out_t ? (p.bn + p.D - 1) / p.D : p.bn;
+    if (per_class <= 96) return launch_general_gn<256, 64>(p, s);
+    return launch_general_gn<128, 128>(p, s);
 }
 
 size_t general_dw_workspace(const DwPass &p) {

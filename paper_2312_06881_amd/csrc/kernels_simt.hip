@@ -31,7 +31,7 @@ struct ColClass {
     __device__ int64_t col(int64_t t) const { return first + t * step; }
 };
 
-__device__ ColClass col_class(const GemmPass &p, int64_t cls) {
+__device__ __forceinline__ ColClass col_class(const GemmPass &p, int64_t cls) {
     ColClass c;
     const int64_t D = p.D;
     if (!p.out_t) {
@@ -91,7 +91,7 @@ __global__ void __launch_bounds__(256) general_gemm_kernel(GemmPass p, int64_t c
     }
     const int64_t a_col1 = cc.g1 * bk;                     // BlockDiag input column at k = 0
     float ra[4], rb[4];
-    auto fetch = [&](int64_t c0) {
+    auto fetch = [&](int64_t c0) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int64_t kq = c0 + a_kk[q];
@@ -114,7 +114,7 @@ __global__ void __launch_bounds__(256) general_gemm_kernel(GemmPass p, int64_t c
             rb[q] = w;
         }
     };
-    auto stash = [&](int buf) {
+    auto stash = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = tid + 256 * q;
@@ -195,7 +195,7 @@ __global__ void __launch_bounds__(256) general_dw_kernel(DwPass p, int64_t jt_n,
     const int64_t chunks = (p.M + kKC - 1) / kKC;
 
     float ra[4], rb[4];
-    auto fetch = [&](int64_t c0) {
+    auto fetch = [&](int64_t c0) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = tid + 256 * q;
@@ -213,7 +213,7 @@ __global__ void __launch_bounds__(256) general_dw_kernel(DwPass p, int64_t jt_n,
             rb[q] = vb;
         }
     };
-    auto stash = [&](int buf) {
+    auto stash = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = tid + 256 * q;
