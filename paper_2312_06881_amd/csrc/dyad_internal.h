@@ -58,8 +58,6 @@ struct DwPass {
 // General kernels: any shape, any D, both dtypes (vector ALU, tiled).
 hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t s);
 hipError_t launch_simt_dw(const DwPass &p, hipStream_t s);
-// db alone (fixed-order token sums), as the general weight-gradient paths use it.
-hipError_t launch_db(const DwPass &p, hipStream_t s);
 
 // General weight gradient on the matrix cores (bf16, any shape), token splits
 // summed in order through the workspace: general_dw_workspace() bytes (0 when

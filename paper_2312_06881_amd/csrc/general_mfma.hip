@@ -248,17 +248,25 @@ __global__ void __launch_bounds__(256, 2) general_mfma_kernel(GemmPass p, int co
     }
 }
 
-// One split's tile of dW: rows j (dZ side), columns k (X side), K = tokens.
-__global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int jt_n, int kt_n, int splits,
+// One split's tile of dW for one component: rows j (dZ side), columns k (X
+// side), K = tokens.  Operands sit in LDS token-major (one 272-byte row of 128
+// entry columns per token, 16 bytes of pad) and the MFMA operands -- 8 tokens
+// of one column per lane -- come from ds_read_b64_tr_b16.  ZP / XP: the
+// operand's columns are contiguous with even offsets, so column pairs are one
+// aligned 4-byte load.
+constexpr int kDwPitch = 128 * 2 + 16;   // bytes per token row
+
+template <bool ZP, bool XP>
+__global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int comp, int jt_n, int kt_n, int splits,
                                                                  int64_t tps, float *part) {
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][kGM * kStageK];   // [buffer][dZ, X]
+    __shared__ __attribute__((aligned(16))) unsigned char lds[2][2][kStageK * kDwPitch];   // [buffer][dZ, X]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int b = blockIdx.x;
-    const int kt = b % kt_n, jt = (b / kt_n) % jt_n, gc = (b / (kt_n * jt_n)) % (2 * (int)p.D);
-    const int split = b / (kt_n * jt_n * 2 * (int)p.D);
-    const int D = (int)p.D, comp = gc < D ? 1 : 2, g = gc % D;
+    const int D = (int)p.D;
+    const int kt = b % kt_n, jt = (b / kt_n) % jt_n, g = (b / (kt_n * jt_n)) % D;
+    const int split = b / (kt_n * jt_n * D);
     const int bo = (int)p.bo, bi = (int)p.bi, n_out = (int)p.n_out, n_in = (int)p.n_in;
-    const int j0 = jt * kGM, k0 = kt * kGN;
+    const int j0 = jt * 128, k0 = kt * 128;
     const bool row_t = comp == 2 && p.out_t, col_t = comp == 2 && p.in_t;
     const int64_t m_lo = (int64_t)split * tps;
     const int64_t m_hi = min(m_lo + tps, p.M);
@@ -270,42 +278,57 @@ __global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int j
     const __amdgpu_buffer_rsrc_t rX =
         buffer_rsrc(static_cast<const uint16_t *>(p.X) + m_lo * p.n_in, (uint32_t)rows * (uint32_t)n_in * 2u);
 
-    // pair q: entry column (j or k) pi % 128, token pair pi / 128
-    int zcol[kPairs], xcol[kPairs], mp[kPairs], ec[kPairs];
+    // pair q: entry columns 2 cp, 2 cp + 1 of token row mm of the chunk
+    int cp[kPairs], mm[kPairs], zc[kPairs][2], xc[kPairs][2];
 #pragma unroll
     for (int q = 0; q < kPairs; ++q) {
         const int pi = tid + 256 * q;
-        ec[q] = pi & (kGM - 1);
-        mp[q] = pi >> 7;
-        const int j = j0 + ec[q], k = k0 + ec[q];
-        const int row = row_t ? j * D + g : g * bo + j;
-        const int col = col_t ? k * D + g : g * bi + k;
-        zcol[q] = (j < bo && row < n_out) ? row : -1;
-        xcol[q] = (k < bi && col < n_in) ? col : -1;
+        cp[q] = pi & 63;
+        mm[q] = pi >> 6;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int j = j0 + 2 * cp[q] + h, k = k0 + 2 * cp[q] + h;
+            const int row = row_t ? j * D + g : g * bo + j;
+            const int col = col_t ? k * D + g : g * bi + k;
+            zc[q][h] = (j < bo && row < n_out) ? row : -1;
+            xc[q][h] = (k < bi && col < n_in) ? col : -1;
+        }
     }
-    uint32_t rz[kPairs][2], rx[kPairs][2];
+    uint32_t rz[kPairs], rx[kPairs];
     auto fetch = [&](int c) __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < kPairs; ++q)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const uint32_t m = (uint32_t)(c * kStageK + 2 * mp[q] + h);
-                rz[q][h] = ld2(rZ, zcol[q] >= 0 ? (m * (uint32_t)n_out + (uint32_t)zcol[q]) * 2u : kNoLoad);
-                rx[q][h] = ld2(rX, xcol[q] >= 0 ? (m * (uint32_t)n_in + (uint32_t)xcol[q]) * 2u : kNoLoad);
-            }
+        for (int q = 0; q < kPairs; ++q) {
+            const uint32_t m = (uint32_t)(c * kStageK + mm[q]);
+            auto off = [&](int col, int width) __attribute__((always_inline)) -> uint32_t {
+                return col >= 0 ? (m * (uint32_t)width + (uint32_t)col) * 2u : kNoLoad;
+            };
+            if constexpr (ZP) rz[q] = ld4(rZ, off(zc[q][0], n_out));
+            else rz[q] = ld2(rZ, off(zc[q][0], n_out)) | (ld2(rZ, off(zc[q][1], n_out)) << 16);
+            if constexpr (XP) rx[q] = ld4(rX, off(xc[q][0], n_in));
+            else rx[q] = ld2(rX, off(xc[q][0], n_in)) | (ld2(rX, off(xc[q][1], n_in)) << 16);
+        }
     };
     auto stash = [&](int buf) __attribute__((always_inline)) {
-        uint16_t *Z = lds[buf][0], *Xs = lds[buf][1];
 #pragma unroll
         for (int q = 0; q < kPairs; ++q) {
-            const int off = lds_off(ec[q], mp[q] >> 2) + (mp[q] & 3) * 2;
-            *reinterpret_cast<uint32_t *>(Z + off) = rz[q][0] | (rz[q][1] << 16);
-            *reinterpret_cast<uint32_t *>(Xs + off) = rx[q][0] | (rx[q][1] << 16);
+            const int off = mm[q] * kDwPitch + 4 * cp[q];
+            *reinterpret_cast<uint32_t *>(lds[buf][0] + off) = rz[q];
+            *reinterpret_cast<uint32_t *>(lds[buf][1] + off) = rx[q];
         }
     };
 
     const int wm0 = (wave >> 1) * 64, wn0 = (wave & 1) * 64;
     const int lr = lane & 15, lc = lane >> 4;
+    // transpose-read lane offsets: token row 8*(lane/16) + (lane%16)/4, column 4*(lane%4)
+    const int trow = 8 * lc + (lr >> 2), tcol = 4 * (lane & 3);
+    // db rides on the BlockDiag items of the first column tile: their dZ
+    // fragments times a fragment of ones (one wave column, so once per row)
+    const bool do_db = p.db && comp == 1 && kt == 0 && (wave & 1) == 0;
+    const bf16x8_t ones = {(__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f,
+                           (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f, (__bf16)1.0f};
+    f32x4_t dacc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dacc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     f32x4_t acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -319,13 +342,17 @@ __global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int j
     for (int c = 0; c < chunks; ++c) {
         const int buf = c & 1;
         if (c + 1 < chunks) fetch(c + 1);
-        const uint16_t *Z = lds[buf][0], *Xs = lds[buf][1];
+        const lds_u8 *Z = (const lds_u8 *)lds[buf][0], *Xs = (const lds_u8 *)lds[buf][1];
         bf16x8_t af[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8_t *>(Z + lds_off(wm0 + 16 * i + lr, lc));
+        for (int i = 0; i < 4; ++i) af[i] = frag_tr(Z + trow * kDwPitch + (wm0 + 16 * i + tcol) * 2, kDwPitch);
+        if (do_db) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dacc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], ones, dacc[i], 0, 0, 0);
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const bf16x8_t bf = *reinterpret_cast<const bf16x8_t *>(Xs + lds_off(wn0 + 16 * j + lr, lc));
+            const bf16x8_t bf = frag_tr(Xs + trow * kDwPitch + (wn0 + 16 * j + tcol) * 2, kDwPitch);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf, acc[i][j], 0, 0, 0);
@@ -352,16 +379,36 @@ __global__ void __launch_bounds__(256, 2) general_mfma_dw_kernel(DwPass p, int j
                 else dW[e] = f32_to_bf16(acc[i][jj][v]);
             }
         }
+    if (do_db && lr == 0) {
+        float *dst_db = part ? part + (int64_t)splits * 2 * per_comp + (int64_t)split * n_out : nullptr;
+        uint16_t *db = static_cast<uint16_t *>(p.db);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int j = j0 + wm0 + 16 * i + 4 * lc + v;
+                const int f = g * bo + j;
+                if (j >= bo || f >= n_out) continue;
+                if (dst_db) dst_db[f] = dacc[i][v];
+                else db[f] = f32_to_bf16(dacc[i][v]);
+            }
+    }
 }
 
-// dW = sum of the splits' partials, in split order.
+// dW (and db) = sum of the splits' partials, in split order.  Partials:
+// [split][2 * per_comp] for dW1, dW2, then [split][n_out] for db.
 __global__ void __launch_bounds__(256) general_dw_reduce(const float *part, int splits, int64_t per_comp,
-                                                         uint16_t *dW1, uint16_t *dW2) {
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per_comp;
+                                                         int64_t n_out, uint16_t *dW1, uint16_t *dW2,
+                                                         uint16_t *db) {
+    const int64_t n_db = db ? n_out : 0;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < 2 * per_comp + n_db;
          e += (int64_t)gridDim.x * blockDim.x) {
+        const bool is_db = e >= 2 * per_comp;
+        const float *src = is_db ? part + (int64_t)splits * 2 * per_comp + (e - 2 * per_comp) : part + e;
+        const int64_t stride = is_db ? n_out : 2 * per_comp;
         float s = 0.f;
-        for (int q = 0; q < splits; ++q) s += part[(int64_t)q * 2 * per_comp + e];
-        uint16_t *out = e < per_comp ? dW1 + e : dW2 + (e - per_comp);
+        for (int q = 0; q < splits; ++q) s += src[(int64_t)q * stride];
+        uint16_t *out = is_db ? db + (e - 2 * per_comp) : (e < per_comp ? dW1 + e : dW2 + (e - per_comp));
         *out = f32_to_bf16(s);
     }
 }
@@ -378,8 +425,11 @@ bool gen_dw_plan(const DwPass &p, GenDwPlan &pl) {
     pl.kt = (int)((p.bi + kGN - 1) / kGN);
     const int64_t tiles = 2 * p.D * pl.jt * pl.kt;
     if (tiles >= ((int64_t)1 << 30)) return false;
-    // enough work items for two workgroups per CU, each at least 256 tokens deep
-    int64_t splits = tiles >= 512 ? 1 : (512 + tiles - 1) / tiles;
+    // each workgroup walks its tokens one 32-token chunk at a time with one
+    // chunk in flight, so it is latency-bound: split the tokens until there
+    // are ~2048 work items (8 per CU; measured best of 512-4096 at OPT-125m
+    // widths, n_dyad 3, 5, 6), each at least 256 tokens deep
+    int64_t splits = tiles >= 2048 ? 1 : (2048 + tiles - 1) / tiles;
     const int64_t max_splits = p.M / 256 > 0 ? p.M / 256 : 1;
     if (splits > max_splits) splits = max_splits;
     int64_t tps = (p.M + splits - 1) / splits;
@@ -437,7 +487,7 @@ hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s) {
 size_t general_dw_workspace(const DwPass &p) {
     GenDwPlan pl;
     if (!gen_dw_plan(p, pl) || pl.splits == 1) return 0;
-    return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi) * sizeof(float);
+    return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi + p.n_out) * sizeof(float);
 }
 
 hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s) {
@@ -446,23 +496,33 @@ hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s) {
     const int64_t per_comp = p.D * p.bo * p.bi;
     float *part = nullptr;
     if (pl.splits > 1) {
-        if (!p.ws || p.ws_bytes < (size_t)pl.splits * (size_t)(2 * per_comp) * sizeof(float))
+        if (!p.ws || p.ws_bytes < (size_t)pl.splits * (size_t)(2 * per_comp + p.n_out) * sizeof(float))
             return hipErrorInvalidValue;
         part = static_cast<float *>(p.ws);
     }
-    const int64_t blocks = (int64_t)pl.splits * 2 * p.D * pl.jt * pl.kt;
-    general_mfma_dw_kernel<<<(unsigned)blocks, 256, 0, s>>>(p, pl.jt, pl.kt, pl.splits, pl.tps, part);
-    hipError_t e = hipGetLastError();
+    // one launch per component: its operands' pair-load forms are fixed per launch
+    const int64_t blocks = (int64_t)pl.splits * p.D * pl.jt * pl.kt;
+    const bool z_ok = p.n_out % 2 == 0 && p.bo % 2 == 0, x_ok = p.n_in % 2 == 0 && p.bi % 2 == 0;
+    hipError_t e = hipSuccess;
+    for (int comp = 1; comp <= 2 && e == hipSuccess; ++comp) {
+        const bool zp = z_ok && !(comp == 2 && p.out_t), xp = x_ok && !(comp == 2 && p.in_t);
+        if (zp && xp) general_mfma_dw_kernel<true, true><<<(unsigned)blocks, 256, 0, s>>>(p, comp, pl.jt, pl.kt, pl.splits, pl.tps, part);
+        else if (zp) general_mfma_dw_kernel<true, false><<<(unsigned)blocks, 256, 0, s>>>(p, comp, pl.jt, pl.kt, pl.splits, pl.tps, part);
+        else if (xp) general_mfma_dw_kernel<false, true><<<(unsigned)blocks, 256, 0, s>>>(p, comp, pl.jt, pl.kt, pl.splits, pl.tps, part);
+        else general_mfma_dw_kernel<false, false><<<(unsigned)blocks, 256, 0, s>>>(p, comp, pl.jt, pl.kt, pl.splits, pl.tps, part);
+        e = hipGetLastError();
+    }
     if (e != hipSuccess) return e;
     if (part) {
-        int64_t grid = (2 * per_comp + 255) / 256;
+        int64_t grid = (2 * per_comp + p.n_out + 255) / 256;
         if (grid > 4096) grid = 4096;
-        general_dw_reduce<<<(unsigned)grid, 256, 0, s>>>(part, pl.splits, per_comp, static_cast<uint16_t *>(p.dW1),
-                                                         static_cast<uint16_t *>(p.dW2));
+        general_dw_reduce<<<(unsigned)grid, 256, 0, s>>>(part, pl.splits, per_comp, p.n_out,
+                                                         static_cast<uint16_t *>(p.dW1),
+                                                         static_cast<uint16_t *>(p.dW2),
+                                                         static_cast<uint16_t *>(p.db));
         e = hipGetLastError();
-        if (e != hipSuccess) return e;
     }
-    return launch_db(p, s);
+    return e;
 }
 
 }  // namespace dyad

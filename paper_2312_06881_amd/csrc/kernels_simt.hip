@@ -14,8 +14,9 @@
 // columns past Nout do not exist.
 //
 // Weight gradient.  dWc[g][j][k] = sum_m dZ[m][row_c(g, j)] X[m][col_c(g, k)]:
-// per (component, group) a GEMM of bo x bi over K = M tokens, tiled 64 x 64.
-// Token sums run in a fixed order.
+// per (component, group) a GEMM of bo x bi over K = M tokens, tiled 64 x 64;
+// the BlockDiag tiles of the first column tile also sum their dZ columns for
+// db.  Token sums run in a fixed order.
 #include "dyad_device.h"
 #include "dyad_internal.h"
 
@@ -193,6 +194,10 @@ __global__ void __launch_bounds__(256) general_dw_kernel(DwPass p, int64_t jt_n,
     const int64_t j0 = jt * kT, k0 = kt * kT;
     const bool row_t = comp == 2 && p.out_t, col_t = comp == 2 && p.in_t;
     const int64_t chunks = (p.M + kKC - 1) / kKC;
+    // db[g*bo + j] = sum_m dZ[m][g*bo + j] is the BlockDiag tile's own dZ column
+    // sum: the first column tile's threads of column 0 add up their A values
+    const bool do_db = p.db && comp == 1 && kt == 0;
+    float dbs[4] = {0.f, 0.f, 0.f, 0.f};
 
     float ra[4], rb[4];
     auto fetch = [&](int64_t c0) __attribute__((always_inline)) {
@@ -246,11 +251,20 @@ __global__ void __launch_bounds__(256) general_dw_kernel(DwPass p, int64_t jt_n,
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], bv[j], acc[i][j]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dbs[i] += a[i];
         }
         if (c + 1 < chunks) stash(buf ^ 1);
         __syncthreads();
     }
 
+    if (do_db && tx == 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t j = j0 + ty + 16 * i, f = g * p.bo + j;
+            if (j < p.bo && f < p.n_out) store_f32(static_cast<T *>(p.db), f, dbs[i]);
+        }
+    }
     T *dW = static_cast<T *>(comp == 1 ? p.dW1 : p.dW2);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -262,26 +276,6 @@ __global__ void __launch_bounds__(256) general_dw_kernel(DwPass p, int64_t jt_n,
             if (k >= p.bi) continue;
             store_f32(dW, (g * p.bo + j) * p.bi + k, acc[i][jj]);
         }
-    }
-}
-
-// db[f] = sum_m dZ[m][f]: 64 columns per block, 16 token lanes per column,
-// summed in a fixed order.
-template <typename T>
-__global__ void __launch_bounds__(1024) general_db_kernel(DwPass p) {
-    __shared__ float part[16][kT + 1];
-    const T *dZ = static_cast<const T *>(p.dZ);
-    const int tx = threadIdx.x & (kT - 1), ty = threadIdx.x / kT;
-    const int64_t f = (int64_t)blockIdx.x * kT + tx;
-    float s = 0.f;
-    if (f < p.n_out)
-        for (int64_t m = ty; m < p.M; m += 16) s += load_f32(dZ, m * p.n_out + f);
-    part[ty][tx] = s;
-    __syncthreads();
-    if (ty == 0 && f < p.n_out) {
-        float t = 0.f;
-        for (int i = 0; i < 16; ++i) t += part[i][tx];
-        store_f32(static_cast<T *>(p.db), f, t);
     }
 }
 
@@ -310,18 +304,6 @@ hipError_t launch_simt_dw(const DwPass &p, hipStream_t s) {
         general_dw_kernel<float><<<(unsigned)blocks, 256, 0, s>>>(p, jt, kt);
     else
         general_dw_kernel<uint16_t><<<(unsigned)blocks, 256, 0, s>>>(p, jt, kt);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_db(p, s);
-}
-
-hipError_t launch_db(const DwPass &p, hipStream_t s) {
-    if (!p.db) return hipSuccess;
-    const int64_t fb = (p.n_out + kT - 1) / kT;
-    if (p.dtype == kF32)
-        general_db_kernel<float><<<(unsigned)fb, 1024, 0, s>>>(p);
-    else
-        general_db_kernel<uint16_t><<<(unsigned)fb, 1024, 0, s>>>(p);
     return hipGetLastError();
 }
 

@@ -110,6 +110,6 @@ def test_backward_dw_rejects_and_workspace_size():
     # padded widths run on the general kernels: in bf16 the matrix-core one splits
     # the tokens through the workspace, in fp32 the vector one needs none
     w5 = dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 1)
-    assert w5 > 0 and w5 % (4 * 2 * 5 * 615 * 154) == 0
+    assert w5 > 0 and w5 % (4 * (2 * 5 * 615 * 154 + 3072)) == 0
     assert dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 0) == 0
     assert dy.dyad_dw_workspace_bytes(9, 768, 3072, 4, 16384, 1) == 0
