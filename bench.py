@@ -34,7 +34,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="opt125m_ff")
+    ap.add_argument("--workload", default="opt125m_ff",
+                    help="opt125m_ff (default), opt350m_ff, sweep_d{1024,2048,4096,8192}_D{2,4,8,16}, "
+                         "wide_M{16,256,32768}, opt125m_ff_D{3,5,6} (n_dyad 5: zero-padded blocks), tiny_it_f32")
     ap.add_argument("--variants", default="IT,OT,DT")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
