@@ -1,0 +1,41 @@
+"""The benchmark's command-line contract: one JSON line with the fields the
+driver reads, and a refusal of more than one GPU (this build runs on one)."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def run_bench(*args, timeout=300):
+    return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True,
+                          text=True, timeout=timeout, cwd=ROOT)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = run_bench("--gpus", "2")
+    assert r.returncode == 2
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    assert line["n_gpus"] == 2 and "one GPU" in line["error"]
+
+
+@pytest.mark.gpu
+def test_bench_json_line():
+    r = run_bench("--steps", "2", "--warmup", "1", "--no-cpu", "--no-dense")
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+              "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"):
+        assert k in d, k
+    assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1
+    assert d["value"] > 0 and d["ms_per_step"] > 0 and d["higher_is_better"] is True
+    assert d["config"]["workload"] == "opt125m_ff"
+    rl = d["roofline"]
+    assert rl["bound"] in ("hbm", "mfma") and rl["peak"] > 0 and 0 < rl["frac"] <= 1
+    assert abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-3
+    assert d["cpu_baseline"] is None
