@@ -2,8 +2,8 @@
 //
 // One workgroup computes an output tile of BM tokens x BN output features.
 // Both weight components run in one K loop (the tile's accumulators take the
-// BlockDiag product first, then the BlockTrans product), so neither partial
-// result leaves registers and no add or concatenation is materialised.
+// BlockDiag and the BlockTrans products), so neither partial result leaves
+// registers and no add or concatenation is materialised.
 //
 // Tile columns.  The BN columns lie in one output block g1, which fixes the
 // BlockDiag weight rows.  Without an output transpose the BlockTrans component
@@ -15,7 +15,8 @@
 // undoes the order.
 //
 // Pipeline.  The K loop runs over stages of 32 k values (one MFMA K step),
-// BlockDiag stages first.  LDS holds two stage buffers: while the waves
+// BlockDiag stages first (with PF = 2 the components alternate and loads run
+// one stage further ahead; see the main loop).  LDS holds two stage buffers: while the waves
 // multiply out of one, the next stage's operands (already in registers) are
 // written into the other and the loads for the stage after that are issued,
 // so global latency hides behind a stage of MFMAs and there is one barrier per
