@@ -41,10 +41,13 @@ int run_gemm(const GemmPass &p, hipStream_t s) {
 }
 
 // Workspace of the weight-gradient path the call will take: the MFMA kernels
-// for shapes they cover, else the general matrix-core kernel.
+// for shapes they cover, else the general matrix-core kernel (bf16), else the
+// general vector kernel.
 size_t dw_workspace(const DwPass &p) {
     const size_t w = dyad::mfma_dw_workspace(p);
-    return w ? w : dyad::general_dw_workspace(p);
+    if (w) return w;
+    if (dyad::general_dw_ok(p)) return dyad::general_dw_workspace(p);
+    return dyad::simt_dw_workspace(p);
 }
 
 }  // namespace

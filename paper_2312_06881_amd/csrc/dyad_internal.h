@@ -55,13 +55,17 @@ struct DwPass {
     size_t ws_bytes;
 };
 
-// General kernels: any shape, any D, both dtypes (vector ALU, tiled).
+// General kernels: any shape, any D, both dtypes (vector ALU, tiled).  The
+// weight gradient splits the tokens through the workspace when the tiles alone
+// would leave the GPU idle: simt_dw_workspace() bytes (0 for one split).
 hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t s);
+size_t simt_dw_workspace(const DwPass &p);
 hipError_t launch_simt_dw(const DwPass &p, hipStream_t s);
 
 // General weight gradient on the matrix cores (bf16, any shape), token splits
 // summed in order through the workspace: general_dw_workspace() bytes (0 when
 // one split suffices or the path does not apply).
+bool general_dw_ok(const DwPass &p);
 size_t general_dw_workspace(const DwPass &p);
 hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s);
 

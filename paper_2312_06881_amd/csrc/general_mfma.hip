@@ -484,6 +484,11 @@ hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s) {
     return launch_general_gn<128, 128>(p, s);
 }
 
+bool general_dw_ok(const DwPass &p) {
+    GenDwPlan pl;
+    return gen_dw_plan(p, pl);
+}
+
 size_t general_dw_workspace(const DwPass &p) {
     GenDwPlan pl;
     if (!gen_dw_plan(p, pl) || pl.splits == 1) return 0;

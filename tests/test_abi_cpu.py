@@ -107,9 +107,10 @@ def test_backward_dw_rejects_and_workspace_size():
     assert dy.dyad_backward_dw(**dict(a, dW2=None)) == -1
     assert dy.dyad_backward_dw(**dict(a, X=FAKE + 1)) == -3
     assert dy.dyad_backward_dw(**dict(a, n_dyad=5, X=FAKE + 1)) == -3   # padded widths pass the shape check
-    # padded widths run on the general kernels: in bf16 the matrix-core one splits
-    # the tokens through the workspace, in fp32 the vector one needs none
-    w5 = dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 1)
-    assert w5 > 0 and w5 % (4 * (2 * 5 * 615 * 154 + 3072)) == 0
-    assert dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 0) == 0
+    # padded widths run on the general kernels, which split the tokens through
+    # the workspace: fp32 partials of dW1, dW2 and db per split
+    per_split = 4 * (2 * 5 * 615 * 154 + 3072)
+    for dtype in (0, 1):
+        w5 = dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, dtype)
+        assert w5 > 0 and w5 % per_split == 0
     assert dy.dyad_dw_workspace_bytes(9, 768, 3072, 4, 16384, 1) == 0
