@@ -106,18 +106,18 @@ OPT350M = Workload("opt350m_ff", d=1024, ffn=4096, n_dyad=4, M=16384,
 
 
 def sweep(d: int, n_dyad: int) -> Workload:
-    """Width/block sweep point: ffn = 4d, M = 16384, Dyad-DT."""
+    """Width/block sweep point: ffn = 4d, M = 16384."""
     return Workload(f"sweep_d{d}_D{n_dyad}", d=d, ffn=4 * d, n_dyad=n_dyad, M=16384,
-                    variants=("DT",), note=f"sweep d={d}, ffn={4 * d}, n_dyad={n_dyad}, DT")
+                    note=f"sweep d={d}, ffn={4 * d}, n_dyad={n_dyad}")
 
 
 SWEEP = [sweep(d, D) for d in (1024, 2048, 4096, 8192) for D in (2, 4, 8, 16)]
 
 
 def wide(M: int) -> Workload:
-    """Wide layer d=8192 -> 32768, n_dyad=16, Dyad-IT."""
-    return Workload(f"wide_M{M}", d=8192, ffn=32768, n_dyad=16, M=M, variants=("IT",),
-                    note=f"wide fc1 8192->32768, n_dyad=16, M={M}, IT")
+    """Wide FF pair 8192 -> 32768 -> 8192, n_dyad=16, M tokens (16 and 256: decode-sized)."""
+    return Workload(f"wide_M{M}", d=8192, ffn=32768, n_dyad=16, M=M,
+                    note=f"wide FF 8192->32768->8192, n_dyad=16, M={M}")
 
 
 WIDE = [wide(M) for M in (16, 256, 32768)]
