@@ -50,6 +50,8 @@ struct DwArgs {
     const uint16_t *dZ, *X;
     float *part;          // [splits][2][D][bo][bi]
     float *part_db;       // [splits][n_out]
+    uint16_t *dW1, *dW2, *db;
+    int direct;           // one split: the tiles store bf16 results, no partials
     int64_t tokens_per_split;
     int tiles_j, tiles_k; // BJ x BK tiles per (component, group)
     int splits, items;    // items = splits * 2 * D * tiles_j * tiles_k
@@ -339,29 +341,46 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         }
     }
 
-    // partial sums -> workspace [split][comp][g][j][k]
+    // one split: bf16 results straight to dW1 / dW2 / db; else fp32 partial
+    // sums -> workspace [split][comp][g][j][k], added by dyad_dw_reduce
     const int gout = MG ? gw : g;
     const int64_t per_comp = (int64_t)D * bo * bi;
-    float *dst = a.part + ((int64_t)split * 2 + (C2 ? 1 : 0)) * per_comp + (int64_t)gout * bo * bi;
+    if (a.direct) {
+        uint16_t *dst = (C2 ? a.dW2 : a.dW1) + (int64_t)gout * bo * bi;
 #pragma unroll
-    for (int i = 0; i < C::kSubJ; ++i)
+        for (int i = 0; i < C::kSubJ; ++i)
 #pragma unroll
-        for (int j = 0; j < C::kSubK; ++j)
+            for (int j = 0; j < C::kSubK; ++j)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int jj = j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
-                const int kk = k0 + wk0 + j * 16 + (lane & 15);
-                dst[(int64_t)jj * bi + kk] = acc[i][j][v];
-            }
+                for (int v = 0; v < 4; ++v) {
+                    const int jj = j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
+                    const int kk = k0 + wk0 + j * 16 + (lane & 15);
+                    dst[(int64_t)jj * bi + kk] = f32_to_bf16(acc[i][j][v]);
+                }
+    } else {
+        float *dst = a.part + ((int64_t)split * 2 + (C2 ? 1 : 0)) * per_comp + (int64_t)gout * bo * bi;
+#pragma unroll
+        for (int i = 0; i < C::kSubJ; ++i)
+#pragma unroll
+            for (int j = 0; j < C::kSubK; ++j)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int jj = j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
+                    const int kk = k0 + wk0 + j * 16 + (lane & 15);
+                    dst[(int64_t)jj * bi + kk] = acc[i][j][v];
+                }
+    }
     if (do_db && (lane & 15) == 0) {
         // every column of a ones-product holds the row sums; lane 16r holds rows 4r..4r+3
 #pragma unroll
         for (int i = 0; i < C::kSubJ; ++i)
             if (i % WKN == wk) {
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    a.part_db[(int64_t)split * a.n_out + g * bo + j0 + wj0 + i * 16 + (lane >> 4) * 4 + v] =
-                        dacc[i / WKN][v];
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t f = g * bo + j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
+                    if (a.direct) a.db[f] = f32_to_bf16(dacc[i / WKN][v]);
+                    else a.part_db[(int64_t)split * a.n_out + f] = dacc[i / WKN][v];
+                }
             }
     }
 }
@@ -419,8 +438,12 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.M = p.M; a.n_in = p.n_in; a.n_out = p.n_out; a.bi = p.bi; a.bo = p.bo;
     a.dZ = static_cast<const uint16_t *>(p.dZ);
     a.X = static_cast<const uint16_t *>(p.X);
-    a.part = static_cast<float *>(p.ws);
-    a.part_db = a.part + (int64_t)pl.splits * 2 * p.D * p.bo * p.bi;
+    a.direct = pl.splits == 1;
+    a.part = a.direct ? nullptr : static_cast<float *>(p.ws);
+    a.part_db = a.direct ? nullptr : a.part + (int64_t)pl.splits * 2 * p.D * p.bo * p.bi;
+    a.dW1 = static_cast<uint16_t *>(p.dW1);
+    a.dW2 = static_cast<uint16_t *>(p.dW2);
+    a.db = static_cast<uint16_t *>(p.db);
     a.tokens_per_split = pl.tokens_per_split;
     a.tiles_j = pl.tiles_j; a.tiles_k = pl.tiles_k;
     a.splits = pl.splits;
@@ -428,7 +451,7 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.want_db = p.db != nullptr;
     dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || a.direct) return e;
     const int64_t per_comp = p.D * p.bo * p.bi;
     const int64_t work = (2 * per_comp + (p.db ? p.n_out : 0)) / 4;
     int64_t grid = (work + 255) / 256;

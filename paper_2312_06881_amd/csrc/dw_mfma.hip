@@ -76,9 +76,14 @@ bool choose(const DwPass &p, DwPlan &pl) {
 
 }  // namespace
 
+bool mfma_dw_ok(const DwPass &p) {
+    DwPlan pl;
+    return choose(p, pl);
+}
+
 size_t mfma_dw_workspace(const DwPass &p) {
     DwPlan pl;
-    if (!choose(p, pl)) return 0;
+    if (!choose(p, pl) || pl.splits == 1) return 0;   // one split writes the results directly
     return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi + p.n_out) * sizeof(float);
 }
 

@@ -34,7 +34,8 @@ bool out_transposed(int v) { return v == DYAD_OT || v == DYAD_DT; }
 int launch_status(hipError_t e) { return e == hipSuccess ? DYAD_OK : DYAD_ERR_LAUNCH; }
 
 int run_gemm(const GemmPass &p, hipStream_t s) {
-    hipError_t e = dyad::launch_mfma_gemm(p, s);
+    hipError_t e = dyad::skinny_ok(p) ? dyad::launch_skinny_gemm(p, s) : hipErrorNotSupported;
+    if (e == hipErrorNotSupported) e = dyad::launch_mfma_gemm(p, s);
     if (e == hipErrorNotSupported) e = dyad::launch_general_mfma_gemm(p, s);
     if (e == hipErrorNotSupported) e = dyad::launch_simt_gemm(p, s);
     return launch_status(e);
@@ -44,8 +45,7 @@ int run_gemm(const GemmPass &p, hipStream_t s) {
 // for shapes they cover, else the general matrix-core kernel (bf16), else the
 // general vector kernel.
 size_t dw_workspace(const DwPass &p) {
-    const size_t w = dyad::mfma_dw_workspace(p);
-    if (w) return w;
+    if (dyad::mfma_dw_ok(p)) return dyad::mfma_dw_workspace(p);
     if (dyad::general_dw_ok(p)) return dyad::general_dw_workspace(p);
     return dyad::simt_dw_workspace(p);
 }
@@ -122,7 +122,7 @@ int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t 
     size_t need = dw_workspace(p);
     if (need > 0 && (!workspace || workspace_bytes < need)) return DYAD_ERR_WORKSPACE;
     p.dZ = dZ; p.X = X; p.dW1 = dW1; p.dW2 = dW2; p.db = dbias; p.ws = workspace; p.ws_bytes = workspace_bytes;
-    hipError_t e = dyad::mfma_dw_workspace(p) > 0 ? dyad::launch_mfma_dw(p, stream) : hipErrorNotSupported;
+    hipError_t e = dyad::mfma_dw_ok(p) ? dyad::launch_mfma_dw(p, stream) : hipErrorNotSupported;
     if (e == hipErrorNotSupported && M > 0) e = dyad::launch_general_mfma_dw(p, stream);
     if (e == hipErrorNotSupported) e = dyad::launch_simt_dw(p, stream);
     return launch_status(e);

@@ -74,14 +74,23 @@ hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s);
 // 32 bits.
 hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s);
 
+// Small-batch grouped GEMM (bf16, at most 32 tokens, widths that n_dyad
+// divides): the reduction split over workgroups, fp32 partial sums in a
+// stream-ordered workspace from a per-device pool, added in a fixed order.
+// hipErrorNotSupported (launching nothing) when skinny_ok() is false.
+bool skinny_ok(const GemmPass &p);
+hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s);
+
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
 // when the pass's shape has no matching tile configuration (zero-padded
 // widths included).
 hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t s);
 
 // MFMA weight gradient (bf16): split over tokens, fixed-order reduction of the
-// splits through the workspace.  mfma_dw_workspace() is 0 when the shape is not
-// covered, and launch_mfma_dw() then returns hipErrorNotSupported.
+// splits through the workspace (mfma_dw_workspace() bytes; 0 when one split
+// covers the tokens and the tiles store the results directly).  When
+// mfma_dw_ok() is false, launch_mfma_dw() returns hipErrorNotSupported.
+bool mfma_dw_ok(const DwPass &p);
 size_t mfma_dw_workspace(const DwPass &p);
 hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s);
 
