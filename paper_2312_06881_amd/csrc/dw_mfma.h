@@ -346,17 +346,28 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     const int gout = MG ? gw : g;
     const int64_t per_comp = (int64_t)D * bo * bi;
     if (a.direct) {
+        // each 16-row slice of the wave's block goes through the wave's own
+        // LDS area (the stage buffers are free after the last barrier) and
+        // leaves as 16-byte row pieces
         uint16_t *dst = (C2 ? a.dW2 : a.dW1) + (int64_t)gout * bo * bi;
+        uint16_t *slice = reinterpret_cast<uint16_t *>(smem) + wave * 16 * C::WK;
+        constexpr int kPieces = 16 * C::WK / 8;
 #pragma unroll
-        for (int i = 0; i < C::kSubJ; ++i)
+        for (int i = 0; i < C::kSubJ; ++i) {
 #pragma unroll
             for (int j = 0; j < C::kSubK; ++j)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int jj = j0 + wj0 + i * 16 + (lane >> 4) * 4 + v;
-                    const int kk = k0 + wk0 + j * 16 + (lane & 15);
-                    dst[(int64_t)jj * bi + kk] = f32_to_bf16(acc[i][j][v]);
-                }
+                for (int v = 0; v < 4; ++v)
+                    slice[((lane >> 4) * 4 + v) * C::WK + j * 16 + (lane & 15)] = f32_to_bf16(acc[i][j][v]);
+#pragma unroll
+            for (int c0 = 0; c0 < kPieces; c0 += 64) {
+                const int c = c0 + lane;
+                if (kPieces % 64 != 0 && c >= kPieces) break;
+                const int r = c / (C::WK / 8), q = c % (C::WK / 8);
+                const uint4 v = *reinterpret_cast<const uint4 *>(slice + r * C::WK + q * 8);
+                *reinterpret_cast<uint4 *>(dst + (int64_t)(j0 + wj0 + i * 16 + r) * bi + k0 + wk0 + q * 8) = v;
+            }
+        }
     } else {
         float *dst = a.part + ((int64_t)split * 2 + (C2 ? 1 : 0)) * per_comp + (int64_t)gout * bo * bi;
 #pragma unroll
@@ -395,6 +406,7 @@ struct DwKernel {
     static constexpr int kLds2 = kMG ? 2 * DwLayout<BJ, BK, D / (kGB ? kGB : 1), kGB ? kGB : 1>::kStageBytes : kLds1;
     static constexpr int kLds = kLds1 > kLds2 ? kLds1 : kLds2;
     static_assert(kLds * C::kMinBlocks <= kDwLdsBudget, "LDS budget");
+    static_assert(kLds >= C::kWaves * 16 * C::WK * 2, "the direct epilogue's slices fit the stage buffers");
 };
 
 template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T>

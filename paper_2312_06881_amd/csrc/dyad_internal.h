@@ -81,6 +81,13 @@ hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s);
 bool skinny_ok(const GemmPass &p);
 hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s);
 
+// Split reductions of the grouped GEMM: a workspace of at least `bytes` for
+// stream s (one per device and stream, kept between calls and regrown in
+// stream order), and the kernel that adds `slices` fp32 partial sums
+// [slices][M][Nout] in slice order and applies the pass's epilogue.
+hipError_t split_workspace(hipStream_t s, size_t bytes, void **out);
+hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s);
+
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
 // when the pass's shape has no matching tile configuration (zero-padded
 // widths included).

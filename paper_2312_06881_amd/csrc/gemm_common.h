@@ -14,17 +14,22 @@ struct GemmArgs {
     int epilogue;
     int tiles_n;        // output tiles per token panel
     int tiles_total;
+    float *part;        // split reduction: fp32 partial sums [splits][M][Nout], else null
+    int splits;         // workgroups along the reduction per tile
 };
 
 // Epilogue of a BM x BN tile whose accumulators sit in the MFMA layout (wave w
 // owns rows (w / WGN) * WM + 16 i + 4 (lane / 16) + v and internal columns
 // wn0 + 16 j + lane % 16).  C supplies kThreads, kWGN, WM, kSubM, kSubN,
 // kEpiRows, kEpiPitch, kEpiElems and kCPR (internal columns per residue with an
-// output transpose).  smem needs 2 * kEpiElems floats and must be free.
+// output transpose).  smem needs 2 * kEpiElems floats and must be free.  With
+// a split reduction (a.part set) the tile's fp32 sums go to slice `split` of
+// the partial sums instead, in real column order and without the epilogue.
 template <class C, int BM, int BN, int D, bool OUT_T>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *smem,
                                               const f32x4_t (&acc)[C::kSubM][C::kSubN], int64_t m0, int n0,
-                                              int64_t rows_left, int tid, int lane, int wave, int wn0) {
+                                              int64_t rows_left, int tid, int lane, int wave, int wn0,
+                                              int split = 0) {
     constexpr int T = C::kThreads;
     auto internal_col = [](int p) -> int { return OUT_T ? (p % D) * C::kCPR + p / D : p; };
     // ---- epilogue: per 16-row MFMA block row, accumulators -> LDS (fp32, in
@@ -40,9 +45,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
     constexpr int kQ = (kGroups + T - 1) / T;            // groups per thread and block row
     constexpr bool kRagged = kGroups % T != 0;
     constexpr int kBiasQ = T % kG8 == 0 ? 1 : kQ;        // passes with distinct columns
-    const bool grad = a.epilogue == kEpiGeluGrad;
-    const bool act = a.epilogue == kEpiBiasGelu;
-    const bool bias = a.bias != nullptr && !grad;
+    const bool partial = a.part != nullptr;
+    const bool grad = !partial && a.epilogue == kEpiGeluGrad;
+    const bool act = !partial && a.epilogue == kEpiBiasGelu;
+    const bool bias = !partial && a.bias != nullptr && a.epilogue != kEpiGeluGrad;
     const bool keep_h = act && a.h_out != nullptr;
     // The tile's rows as buffers: rows past the batch read zero and drop stores.
     const uint32_t rows_t = (uint32_t)(rows_left < BM ? rows_left : BM);
@@ -51,6 +57,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
     const uint16_t *hbase = grad ? a.h_in : a.h_out;
     const __amdgpu_buffer_rsrc_t rH = buffer_rsrc((hbase ? hbase : a.out) + m0 * a.Nout, o_bytes);
     const uint32_t row16 = 16u * (uint32_t)a.Nout * 2u;  // bytes between block rows
+    const __amdgpu_buffer_rsrc_t rP =
+        buffer_rsrc(partial ? a.part + ((int64_t)split * a.M + m0) * a.Nout : nullptr, partial ? 2u * o_bytes : 0u);
 
     uint32_t voE[kQ];
     int c8of[kQ], erof[kQ];
@@ -107,6 +115,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
                 x[4] = hi.x; x[5] = hi.y; x[6] = hi.z; x[7] = hi.w;
             }
             const uint32_t vo = voE[q] + (uint32_t)i * row16;
+            if (partial) {
+                const u32x4_t lo = {__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])};
+                const u32x4_t hi = {__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]), __float_as_uint(x[7])};
+                __builtin_amdgcn_raw_buffer_store_b128(lo, rP, (int)(2u * vo), 0, 0);
+                __builtin_amdgcn_raw_buffer_store_b128(hi, rP, (int)(2u * vo + 16u), 0, 0);
+                continue;
+            }
             if (grad) {
                 const uint4 h = hq[i & 1][q];
 #pragma unroll

@@ -93,13 +93,17 @@ dyad_gemm_mfma(GemmArgs a) {
     uint16_t *lds = reinterpret_cast<uint16_t *>(smem);
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int tile = xcd_tile(blockIdx.x, a.tiles_total);
+    // work item -> (tile, split): the splits of a tile sit next to each other,
+    // on one XCD, where they share the tile's token panel
+    const int item = xcd_tile(blockIdx.x, a.tiles_total * a.splits);
+    const int tile = item / a.splits, split = item % a.splits;
     const int64_t m0 = (int64_t)(tile / a.tiles_n) * BM;
     const int n0 = (tile % a.tiles_n) * BN;        // first output column of the tile
     const int bk = (int)a.bk, bn = (int)a.bn, Kin = (int)a.Kin;
     const int g1 = n0 / bn;                        // output block = BlockDiag group
     const int jb = n0 - g1 * bn;                   // first BlockDiag weight row
-    const int ks = bk / kStageK;                   // stages per component
+    const int ks = bk / kStageK / a.splits;        // stages per component in this split
+    const int kofs = split * ks;                   // first stage of the split, per component
     const int S = 2 * ks;
 
     const int wm0 = (wave / WGN) * C::WM;
@@ -170,7 +174,7 @@ dyad_gemm_mfma(GemmArgs a) {
         constexpr bool C2 = decltype(comp)::value;
         auto &ra = ras[decltype(set)::value];
         auto &rb = rbs[decltype(set)::value];
-        const uint32_t kk = (uint32_t)((C2 ? s - ks : s) * kStageK);
+        const uint32_t kk = (uint32_t)(((C2 ? s - ks : s) + kofs) * kStageK);
 #pragma unroll
         for (int q = 0; q < C::kRC; ++q) {
             if constexpr (!C2 || !(IN_T || OUT_T)) {
@@ -380,7 +384,7 @@ dyad_gemm_mfma(GemmArgs a) {
         __syncthreads();
     }
 
-    gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0);
+    gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
 }
 
 }  // namespace dyad

@@ -74,13 +74,16 @@ dyad_gemm_mfma2(GemmArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int tile = xcd_tile(blockIdx.x, a.tiles_total);
+    // work item -> (tile, split), the splits of a tile next to each other
+    const int item = xcd_tile(blockIdx.x, a.tiles_total * a.splits);
+    const int tile = item / a.splits, split = item % a.splits;
     const int64_t m0 = (int64_t)(tile / a.tiles_n) * BM;
     const int n0 = (tile % a.tiles_n) * BN;        // first output column of the tile
     const int bk = (int)a.bk, bn = (int)a.bn, Kin = (int)a.Kin;
     const int g1 = n0 / bn;                        // output block = BlockDiag group
     const int jb = n0 - g1 * bn;                   // first BlockDiag weight row / column
-    const int S = bk / kStageK;                    // stages (each both components)
+    const int S = bk / kStageK / a.splits;         // stages of this split (each both components)
+    const int kofs = split * S;
 
     const int wm0 = (wave / WGN) * C::WM;
     const int wn0 = (wave % WGN) * C::WN;
@@ -174,7 +177,7 @@ dyad_gemm_mfma2(GemmArgs a) {
 
     // ---- global -> registers: stage s (reduction indices 32 s .. 32 s + 31 of both components)
     auto fetch = [&](int s) {
-        const uint32_t kk = (uint32_t)(s * kStageK);
+        const uint32_t kk = (uint32_t)((s + kofs) * kStageK);
 #pragma unroll
         for (int q = 0; q < C::kQA1; ++q) ra1[q] = bload16(rA, voA1[q], kk * 2u);
 #pragma unroll
@@ -299,7 +302,7 @@ dyad_gemm_mfma2(GemmArgs a) {
         __syncthreads();
     }
 
-    gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0);
+    gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
 }
 
 }  // namespace dyad

@@ -15,6 +15,41 @@ constexpr int occupancy() {
     return (C::kThreads <= 256 && (160 * 1024) / C::kLds >= 2 && acc_per_lane <= 128) ? 2 : 1;
 }
 
+// Splits of the reduction for a launch of `tiles` output tiles: none when the
+// tiles alone fill the GPU; otherwise the fewest that give about 384 work
+// items, each split keeping at least `min_stages` stages per component, and no
+// more than keep the fp32 partial sums (written and read once) within the
+// bytes of the two weight tensors.
+inline int gemm_splits(const GemmPass &p, int64_t tiles, int min_stages) {
+    if (tiles >= 192) return 1;
+    const int ks = (int)(p.bk / kStageK);
+    const int64_t wbytes = 4 * p.D * p.bn * p.bk;
+    int best = 1;
+    for (int sp = 2; sp * min_stages <= ks; ++sp) {
+        if (ks % sp != 0) continue;
+        if ((int64_t)sp * p.M * p.Nout * 8 > wbytes) break;
+        best = sp;
+        if (tiles * sp >= 384) break;
+    }
+    return best;
+}
+
+// Workspace for `splits` partial sums of pass p on stream s; false (and no
+// split) when none can be had.
+inline bool gemm_split_ws(const GemmPass &p, int splits, hipStream_t s, GemmArgs &a) {
+    a.part = nullptr;
+    a.splits = 1;
+    if (splits <= 1) return false;
+    void *ws = nullptr;
+    if (split_workspace(s, (size_t)splits * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    a.part = static_cast<float *>(ws);
+    a.splits = splits;
+    return true;
+}
+
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int PF = 1>
 hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
@@ -39,9 +74,12 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     a.tiles_n = (int)tiles_n;
     a.tiles_total = (int)(tiles_m * tiles_n);
+    gemm_split_ws(p, gemm_splits(p, a.tiles_total, PF), s, a);
     dyad_gemm_mfma<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, occupancy<C>(), PF>
-        <<<a.tiles_total, C::kThreads, 0, s>>>(a);
-    return hipGetLastError();
+        <<<a.tiles_total * a.splits, C::kThreads, 0, s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && a.part) e = launch_split_reduce(p, a.part, a.splits, s);
+    return e;
 }
 
 // Launch of a fused-stage tile (gemm_mfma2.h).
@@ -66,8 +104,11 @@ hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
     if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     a.tiles_n = (int)tiles_n;
     a.tiles_total = (int)(tiles_m * tiles_n);
-    dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T><<<a.tiles_total, C::kThreads, 0, s>>>(a);
-    return hipGetLastError();
+    gemm_split_ws(p, gemm_splits(p, a.tiles_total, 1), s, a);
+    dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T><<<a.tiles_total * a.splits, C::kThreads, 0, s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && a.part) e = launch_split_reduce(p, a.part, a.splits, s);
+    return e;
 }
 
 // Whether a fused-stage tile fits (LDS of Gemm2Cfg, without instantiating it).

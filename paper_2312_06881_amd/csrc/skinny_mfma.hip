@@ -372,7 +372,9 @@ hipError_t pool_of(int dev, hipMemPool_t *out) {
     return hipSuccess;
 }
 
-hipError_t stream_workspace(hipStream_t s, size_t bytes, void **out) {
+}  // namespace
+
+hipError_t split_workspace(hipStream_t s, size_t bytes, void **out) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -402,7 +404,12 @@ hipError_t stream_workspace(hipStream_t s, size_t bytes, void **out) {
     return hipSuccess;
 }
 
-}  // namespace
+hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s) {
+    if (p.Nout % 8 != 0) return hipErrorNotSupported;
+    const int64_t threads = p.M * (p.Nout / 8);
+    skinny_reduce_kernel<<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(p, part, slices);
+    return hipGetLastError();
+}
 
 bool skinny_ok(const GemmPass &p) {
     if (p.dtype != kBF16 || p.M < 1 || p.M > kSkMaxTok) return false;
@@ -436,18 +443,14 @@ hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s) {
     }
     const size_t bytes = (size_t)slices * (size_t)p.M * (size_t)p.Nout * sizeof(float);
     void *ws = nullptr;
-    if (stream_workspace(s, bytes, &ws) != hipSuccess) {
+    if (split_workspace(s, bytes, &ws) != hipSuccess) {
         (void)hipGetLastError();      // no workspace: the tiled kernels take the pass
         return hipErrorNotSupported;
     }
     a.part = static_cast<float *>(ws);
     const bool g2 = a.c[1].gather != 0;
     hipError_t e = p.M <= 16 ? launch_part_mt<1>(a, kr, p.w_t, g2, s) : launch_part_mt<2>(a, kr, p.w_t, g2, s);
-    if (e == hipSuccess) {
-        const int64_t threads = p.M * (p.Nout / 8);
-        skinny_reduce_kernel<<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(p, a.part, slices);
-        e = hipGetLastError();
-    }
+    if (e == hipSuccess) e = launch_split_reduce(p, a.part, slices, s);
     return e;
 }
 
