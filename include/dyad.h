@@ -19,7 +19,7 @@
  * D*bi -> D*bo on X with zero columns appended, and only its first n_out
  * outputs exist.  Entries whose row is >= n_out or whose column is >= n_in
  * have no effect, and their gradients are zero.  Such widths run on the
- * general (non-matrix-core) kernels.
+ * general kernels.
  *
  * Layouts: every activation is token-major and row-major: X[M][n_in],
  * Y, H, dZ [M][n_out], dX, H_in [M][n_in]; W1, W2, dW1, dW2 as above; bias and
@@ -28,10 +28,18 @@
  * bf16 results are rounded to nearest even.
  *
  * Ownership and ordering: the caller allocates and owns every buffer, the
- * dW workspace included; the library keeps no per-call allocation.  Every
- * call only enqueues work on `stream` (NULL = the null stream) and returns
- * without synchronising; results are valid once that work completes.  Outputs
- * are overwritten, never accumulated into.
+ * dW workspace included.  dyad_forward and dyad_backward_dx may split their
+ * reduction over workgroups (small batches, few output tiles); the fp32
+ * partial sums then go to a library-owned device buffer, one per (device,
+ * stream), taken in stream order from a per-device memory pool of the current
+ * device the first time that stream needs it, regrown in stream order when a
+ * later call needs more, and kept until the process ends (at most a few
+ * split slices of M x n_out fp32).  Calls on one stream share it in stream
+ * order; calls on different streams never share it.  When it cannot be had,
+ * the call runs without the split.  Every call only enqueues work on `stream`
+ * (NULL = the null stream) and returns without synchronising; results are
+ * valid once that work completes.  Outputs are overwritten, never accumulated
+ * into.
  *
  * Errors: each call returns DYAD_OK (0) or a negative dyad_status.  All
  * argument checks run before any HIP call, so a rejected call touches no

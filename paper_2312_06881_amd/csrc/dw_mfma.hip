@@ -47,8 +47,10 @@ bool choose(const DwPass &p, DwPlan &pl) {
     // A strided BlockTrans operand wants a configuration with an all-groups
     // layout; without one its items read the whole span per group.  At n_dyad
     // 16 the all-groups tiles (32 x 32 per group) pay off only when both
-    // operands are strided (measured at d = 4096).
-    const bool want_mg = p.D > 1 && (p.in_t || p.out_t) && (p.D < 16 || (p.in_t && p.out_t));
+    // operands are strided (measured at d = 4096), and not for a batch of at
+    // most 64 tokens, where the one-group 256 x 256 tiles measured 43 against
+    // 53 us (wide layer 8192 -> 32768, 16 tokens).
+    const bool want_mg = p.D > 1 && (p.in_t || p.out_t) && (p.D < 16 || (p.in_t && p.out_t && p.M > 64));
     for (int pass = want_mg ? 0 : 1; pass < 2; ++pass)
     for (const Cand &c : kCands) {
         if (p.bo % c.BJ || p.bi % c.BK) continue;

@@ -25,11 +25,11 @@ struct GemmArgs {
 // output transpose).  smem needs 2 * kEpiElems floats and must be free.  With
 // a split reduction (a.part set) the tile's fp32 sums go to slice `split` of
 // the partial sums instead, in real column order and without the epilogue.
-template <class C, int BM, int BN, int D, bool OUT_T>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *smem,
-                                              const f32x4_t (&acc)[C::kSubM][C::kSubN], int64_t m0, int n0,
-                                              int64_t rows_left, int tid, int lane, int wave, int wn0,
-                                              int split = 0) {
+template <class C, int BM, int BN, int D, bool OUT_T, bool PARTIAL>
+__device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned char *smem,
+                                                 const f32x4_t (&acc)[C::kSubM][C::kSubN], int64_t m0, int n0,
+                                                 int64_t rows_left, int tid, int lane, int wave, int wn0,
+                                                 int split) {
     constexpr int T = C::kThreads;
     auto internal_col = [](int p) -> int { return OUT_T ? (p % D) * C::kCPR + p / D : p; };
     // ---- epilogue: per 16-row MFMA block row, accumulators -> LDS (fp32, in
@@ -45,10 +45,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
     constexpr int kQ = (kGroups + T - 1) / T;            // groups per thread and block row
     constexpr bool kRagged = kGroups % T != 0;
     constexpr int kBiasQ = T % kG8 == 0 ? 1 : kQ;        // passes with distinct columns
-    const bool partial = a.part != nullptr;
-    const bool grad = !partial && a.epilogue == kEpiGeluGrad;
-    const bool act = !partial && a.epilogue == kEpiBiasGelu;
-    const bool bias = !partial && a.bias != nullptr && a.epilogue != kEpiGeluGrad;
+    const bool grad = !PARTIAL && a.epilogue == kEpiGeluGrad;
+    const bool act = !PARTIAL && a.epilogue == kEpiBiasGelu;
+    const bool bias = !PARTIAL && a.bias != nullptr && !grad;
     const bool keep_h = act && a.h_out != nullptr;
     // The tile's rows as buffers: rows past the batch read zero and drop stores.
     const uint32_t rows_t = (uint32_t)(rows_left < BM ? rows_left : BM);
@@ -57,8 +56,6 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
     const uint16_t *hbase = grad ? a.h_in : a.h_out;
     const __amdgpu_buffer_rsrc_t rH = buffer_rsrc((hbase ? hbase : a.out) + m0 * a.Nout, o_bytes);
     const uint32_t row16 = 16u * (uint32_t)a.Nout * 2u;  // bytes between block rows
-    const __amdgpu_buffer_rsrc_t rP =
-        buffer_rsrc(partial ? a.part + ((int64_t)split * a.M + m0) * a.Nout : nullptr, partial ? 2u * o_bytes : 0u);
 
     uint32_t voE[kQ];
     int c8of[kQ], erof[kQ];
@@ -115,7 +112,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
                 x[4] = hi.x; x[5] = hi.y; x[6] = hi.z; x[7] = hi.w;
             }
             const uint32_t vo = voE[q] + (uint32_t)i * row16;
-            if (partial) {
+            if constexpr (PARTIAL) {
+                const __amdgpu_buffer_rsrc_t rP = buffer_rsrc(a.part + ((int64_t)split * a.M + m0) * a.Nout, 2u * o_bytes);
                 const u32x4_t lo = {__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])};
                 const u32x4_t hi = {__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]), __float_as_uint(x[7])};
                 __builtin_amdgcn_raw_buffer_store_b128(lo, rP, (int)(2u * vo), 0, 0);
@@ -144,6 +142,18 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *
                                         pack_bf16(x[6], x[7])));
         }
     }
+}
+
+// The epilogue, or with a split reduction (a.part set) the fp32 partial sums:
+// two inlined instances, so the bias / GELU / GELU' path carries no test of it.
+template <class C, int BM, int BN, int D, bool OUT_T>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, unsigned char *smem,
+                                              const f32x4_t (&acc)[C::kSubM][C::kSubN], int64_t m0, int n0,
+                                              int64_t rows_left, int tid, int lane, int wave, int wn0, int split) {
+    if (a.part)
+        gemm_epilogue_as<C, BM, BN, D, OUT_T, true>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
+    else
+        gemm_epilogue_as<C, BM, BN, D, OUT_T, false>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
 }
 
 }  // namespace dyad
