@@ -170,8 +170,12 @@ struct DwSlots {
 };
 
 // One item: component C2, groups g0.. (all groups when MG), tile (jt, kt) in
-// units of the item's per-group JT x KT tile.
-template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool C2, bool MG>
+// units of the item's per-group JT x KT tile.  ONE: the split holds at most
+// one 32-token stage (small batches), which runs straight through -- the
+// pipelined loop would also issue the loads of four stages that read only
+// zeros, and at 16 tokens those loads, not the stores, set the time.  Its own
+// kernel instance, so the pipelined kernel's registers are unaffected.
+template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool C2, bool MG, bool ONE>
 __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, int split, int g, int jt, int kt) {
     using C = DwCfg<BJ, BK, WJN, WKN>;
     constexpr int GB = MG ? mg_gb<D, BJ, BK, WJN, WKN>() : 1;
@@ -321,7 +325,13 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     using Set0 = std::integral_constant<int, 0>;
     using Set1 = std::integral_constant<int, 1>;
     unsigned char *buf0 = smem, *buf1 = smem + L::kStageBytes;
-    if (stages > 0) {
+    if constexpr (ONE) {
+        fetch(Set0{}, 0);
+        stash(Set0{}, buf0);
+        __syncthreads();
+        compute(buf0);
+        __syncthreads();
+    } else if (stages > 0) {
         fetch(Set0{}, 0);
         fetch(Set1{}, 1);
         stash(Set0{}, buf0);
@@ -409,7 +419,7 @@ struct DwKernel {
     static_assert(kLds >= C::kWaves * 16 * C::WK * 2, "the direct epilogue's slices fit the stage buffers");
 };
 
-template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T>
+template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool ONE>
 __global__ void __launch_bounds__(64 * WJN * WKN, (DwCfg<BJ, BK, WJN, WKN>::kMinBlocks))
 dyad_dw_mfma(DwArgs a) {
     using K = DwKernel<D, BJ, BK, WJN, WKN, IN_T, OUT_T>;
@@ -424,12 +434,12 @@ dyad_dw_mfma(DwArgs a) {
         const int kt = t % a.tiles_k;
         const int jt = (t / a.tiles_k) % a.tiles_j;
         const int g = t / (a.tiles_k * a.tiles_j);
-        if (comp == 0) dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false, false>(a, smem, split, g, jt, kt);
-        else dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, false>(a, smem, split, g, jt, kt);
+        if (comp == 0) dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false, false, ONE>(a, smem, split, g, jt, kt);
+        else dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, false, ONE>(a, smem, split, g, jt, kt);
     } else if constexpr (K::kMG) {
         // all groups: (D / GB) * tiles_j x GB * tiles_k tiles of (BJ / GA) x (BK / GB)
         const int nk = K::kGB * a.tiles_k;
-        dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, true>(a, smem, split, 0, t / nk, t % nk);
+        dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, true, ONE>(a, smem, split, 0, t / nk, t % nk);
     }
 }
 
@@ -461,7 +471,10 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.splits = pl.splits;
     a.items = pl.splits * 2 * D * pl.tiles_j * pl.tiles_k;
     a.want_db = p.db != nullptr;
-    dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
+    if (pl.tokens_per_split >= p.M && p.M <= kStageK)   // one split of one stage
+        dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
+    else
+        dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.direct) return e;
     const int64_t per_comp = p.D * p.bo * p.bi;

@@ -1,5 +1,6 @@
-"""GPU parity of the small-batch path (at most 32 tokens): forward and input
-gradient through the C-ABI against the CPU oracle, element by element.
+"""GPU parity of the small-batch paths (at most 32 tokens): forward, input
+gradient and weight / bias gradients through the C-ABI against the CPU
+oracle, element by element.
 
 Shapes are chosen so that every form of that path runs: block slabs and
 gathered residues (n_dyad 2, 3, 4, 8, 16), untransposed and transposed
@@ -81,6 +82,23 @@ def test_backward_dx_few_tokens(shape, variant, act_in, M):
     ref = oracle.backward_dx(variant, n_in, n_out, D, L.f64("dZ"), L.f64("W1"), L.f64("W2"),
                              act_in=ACT[act_in], H_in=L.f64("H_in") if act_in == "gelu" else None)
     assert_close(dx, ref, "bf16", "dX")
+
+
+@pytest.mark.parametrize("M", TOKENS)
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", SHAPES, ids=case_id)
+def test_backward_dw_few_tokens(shape, variant, M):
+    """Weight and bias gradients with at most 32 tokens: one token split, the
+    tiles storing bf16 results directly."""
+    n_in, n_out, D = shape
+    banner("backward_dw", shape, variant, M)
+    L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=M)
+    dw1, dw2, db = dy.backward_dw(gpu(L.dZ), gpu(L.X), D, variant=variant)
+    torch.cuda.synchronize()
+    r1, r2, rb = oracle.backward_dw(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"))
+    assert_close(dw1, r1, "bf16", "dW1")
+    assert_close(dw2, r2, "bf16", "dW2")
+    assert_close(db, rb, "bf16", "db")
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
