@@ -236,12 +236,17 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     // ---- global -> registers: stage s into register set P.  Buffers start at
     // the stage's first token and end at the split's end, so tokens past it
     // read as zero.
-    auto fetch_side = [&](auto side, auto &sl, auto set, __amdgpu_buffer_rsrc_t r) {
+    auto fetch_side = [&](auto side, auto &sl, auto set, __amdgpu_buffer_rsrc_t r, uint32_t rows) {
         using S = decltype(side);
         constexpr int P = decltype(set)::value;
 #pragma unroll
         for (int q = 0; q < S::kSlots; ++q) {
-            if constexpr (S::kKind == 1) {
+            // one-stage splits skip the token rows past the batch (they read zero)
+            // instead of issuing their loads
+            if (ONE && (uint32_t)((tid + q * T) / S::kPerRow) >= rows) {
+#pragma unroll
+                for (int v = 0; v < (S::kKind == 1 ? 1 : S::kVec); ++v) sl.r[P][q][v] = make_uint4(0u, 0u, 0u, 0u);
+            } else if constexpr (S::kKind == 1) {
                 sl.r[P][q][0] = load_strided8<D>(r, sl.vo[q]);
             } else {
 #pragma unroll
@@ -254,8 +259,8 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         const int64_t left = t_end - tok;
         const uint32_t rows = left <= 0 ? 0u : (uint32_t)(left < kStageK ? left : kStageK);
         const int64_t base = left <= 0 ? 0 : tok;
-        fetch_side(SA{}, sa, set, buffer_rsrc(a.dZ + base * a.n_out, rows * n_out * 2u));
-        fetch_side(SB{}, sb, set, buffer_rsrc(a.X + base * a.n_in, rows * n_in * 2u));
+        fetch_side(SA{}, sa, set, buffer_rsrc(a.dZ + base * a.n_out, rows * n_out * 2u), rows);
+        fetch_side(SB{}, sb, set, buffer_rsrc(a.X + base * a.n_in, rows * n_in * 2u), rows);
     };
     // ---- registers -> LDS stage buffer
     auto stash_side = [&](auto side, auto swz, auto &sl, auto set, unsigned char *buf) {

@@ -51,8 +51,14 @@ bool choose(const DwPass &p, DwPlan &pl) {
     // most 64 tokens, where the one-group 256 x 256 tiles measured 43 against
     // 53 us (wide layer 8192 -> 32768, 16 tokens).
     const bool want_mg = p.D > 1 && (p.in_t || p.out_t) && (p.D < 16 || (p.in_t && p.out_t && p.M > 64));
+    // A batch of at most 32 tokens is one stage per tile, bound by the stores of
+    // the result: 256 x 128 tiles on 4 x 2 waves measured best there (wide
+    // layer 8192 -> 32768, n_dyad 16, 16 tokens: 19-24 us against 24-28 us for
+    // 256 x 256), so they go first.
+    const bool one_stage = p.M <= kStageK;
     for (int pass = want_mg ? 0 : 1; pass < 2; ++pass)
-    for (const Cand &c : kCands) {
+    for (int ci = one_stage ? -1 : 0; ci < (int)(sizeof(kCands) / sizeof(kCands[0])); ++ci) {
+        const Cand c = ci < 0 ? Cand{256, 128, 4, 2} : kCands[ci];
         if (p.bo % c.BJ || p.bi % c.BK) continue;
         if (pass == 0 && !dw_mg_available((int)p.D, c.BJ, c.BK, c.WJN, c.WKN)) continue;
         pl.BJ = c.BJ; pl.BK = c.BK; pl.WJN = c.WJN; pl.WKN = c.WKN;
