@@ -14,8 +14,9 @@ struct GemmArgs {
     int epilogue;
     int tiles_n;        // output tiles per token panel
     int tiles_total;
-    float *part;        // split reduction: fp32 partial sums [splits][M][Nout], else null
+    float *part;        // split reduction: fp32 partial sums [slices][M][Nout], else null
     int splits;         // workgroups along the reduction per tile
+    int slice0;         // partial slice of split 0
 };
 
 // Epilogue of a BM x BN tile whose accumulators sit in the MFMA layout (wave w
@@ -113,7 +114,8 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
             }
             const uint32_t vo = voE[q] + (uint32_t)i * row16;
             if constexpr (PARTIAL) {
-                const __amdgpu_buffer_rsrc_t rP = buffer_rsrc(a.part + ((int64_t)split * a.M + m0) * a.Nout, 2u * o_bytes);
+                const __amdgpu_buffer_rsrc_t rP =
+                    buffer_rsrc(a.part + ((int64_t)(a.slice0 + split) * a.M + m0) * a.Nout, 2u * o_bytes);
                 const u32x4_t lo = {__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])};
                 const u32x4_t hi = {__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]), __float_as_uint(x[7])};
                 __builtin_amdgcn_raw_buffer_store_b128(lo, rP, (int)(2u * vo), 0, 0);

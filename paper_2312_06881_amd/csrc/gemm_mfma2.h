@@ -65,7 +65,11 @@ struct Gemm2Cfg {
     static_assert(kLds <= 160 * 1024, "LDS budget");
 };
 
-template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
+// ONLY = 1 or 2: that component alone, into fp32 partial sums (a.part, slice
+// a.slice0).  Component 2 alone under an output transpose needs no output
+// block per tile: its columns f = j*D + g take weight group f % D and row
+// f / D whatever block f falls in.
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY = 0>
 __global__ void __launch_bounds__(64 * WGM * WGN, 1)
 dyad_gemm_mfma2(GemmArgs a) {
     using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
@@ -178,10 +182,12 @@ dyad_gemm_mfma2(GemmArgs a) {
     // ---- global -> registers: stage s (reduction indices 32 s .. 32 s + 31 of both components)
     auto fetch = [&](int s) {
         const uint32_t kk = (uint32_t)((s + kofs) * kStageK);
+        if constexpr (ONLY != 2) {
 #pragma unroll
-        for (int q = 0; q < C::kQA1; ++q) ra1[q] = bload16(rA, voA1[q], kk * 2u);
+            for (int q = 0; q < C::kQA1; ++q) ra1[q] = bload16(rA, voA1[q], kk * 2u);
+        }
 #pragma unroll
-        for (int q = 0; q < C::kQA2; ++q) {
+        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQA2); ++q) {
             if constexpr (IN_T) {
 #pragma unroll
                 for (int d = 0; d < D; ++d) ra2[q][d] = bload16(rA, voA2[q] + d * 16u, kk * D * 2u);
@@ -191,20 +197,20 @@ dyad_gemm_mfma2(GemmArgs a) {
         }
         const uint32_t kb = W_T ? kk * (uint32_t)bn * 2u : kk * 2u;
 #pragma unroll
-        for (int q = 0; q < C::kQB1; ++q)
+        for (int q = 0; q < (ONLY == 2 ? 0 : C::kQB1); ++q)
 #pragma unroll
             for (int d = 0; d < C::kVB1; ++d) rb1[q][d] = bload16(rW1, voB1[q] + d * 16u, kb);
 #pragma unroll
-        for (int q = 0; q < C::kQB; ++q) rb2[q] = bload16(rW2, voB2[q], kb);
+        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQB); ++q) rb2[q] = bload16(rW2, voB2[q], kb);
     };
 
     // ---- registers -> LDS stage buffer
     auto stash = [&](unsigned char *buf) {
 #pragma unroll
-        for (int q = 0; q < C::kQA1; ++q)
+        for (int q = 0; q < (ONLY == 2 ? 0 : C::kQA1); ++q)
             if (C::kRowChunks % T == 0 || okA1[q]) *reinterpret_cast<uint4 *>(buf + loA1[q]) = ra1[q];
 #pragma unroll
-        for (int q = 0; q < C::kQA2; ++q) {
+        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQA2); ++q) {
             if (C::kUnitsA2 % T != 0 && !okA2[q]) continue;
             if constexpr (IN_T) {
                 uint4 span[D];
@@ -219,7 +225,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             }
         }
 #pragma unroll
-        for (int q = 0; q < C::kQB1; ++q) {
+        for (int q = 0; q < (ONLY == 2 ? 0 : C::kQB1); ++q) {
             if (C::kUnitsB1 % T == 0 || okB1[q]) {
                 if constexpr (C::kB1Chunks) {
                     uint4 span[D];
@@ -232,7 +238,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             }
         }
 #pragma unroll
-        for (int q = 0; q < C::kQB; ++q)
+        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQB); ++q)
             if (C::kUnitsB % T == 0 || okB2[q]) *reinterpret_cast<uint4 *>(buf + loB2[q]) = rb2[q];
     };
 
@@ -247,18 +253,20 @@ dyad_gemm_mfma2(GemmArgs a) {
     };
     auto compute = [&](const unsigned char *buf) {
         bf16x8_t afrag[C::kSubM];
-#pragma unroll
-        for (int i = 0; i < C::kSubM; ++i)
-            afrag[i] = *reinterpret_cast<const bf16x8_t *>(buf + lds_off(wm0 + i * 16 + lr, lc) * 2);
-#pragma unroll
-        for (int j = 0; j < C::kSubN; ++j) {
-            const bf16x8_t bf = bfrag(buf + C::kOffB1, j);
+        if constexpr (ONLY != 2) {
 #pragma unroll
             for (int i = 0; i < C::kSubM; ++i)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag[i], bf, acc[i][j], 0, 0, 0);
+                afrag[i] = *reinterpret_cast<const bf16x8_t *>(buf + lds_off(wm0 + i * 16 + lr, lc) * 2);
+#pragma unroll
+            for (int j = 0; j < C::kSubN; ++j) {
+                const bf16x8_t bf = bfrag(buf + C::kOffB1, j);
+#pragma unroll
+                for (int i = 0; i < C::kSubM; ++i)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag[i], bf, acc[i][j], 0, 0, 0);
+            }
         }
 #pragma unroll
-        for (int rr = 0; rr < C::kRPW; ++rr) {
+        for (int rr = 0; rr < (ONLY == 1 ? 0 : C::kRPW); ++rr) {
             const int r = OUT_T ? (wn0 + rr * C::kCPR) / C::kCPR : 0;
             const unsigned char *slab = buf + C::kOffA2 + r * C::kSlab;
 #pragma unroll

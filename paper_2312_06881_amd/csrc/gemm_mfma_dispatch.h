@@ -39,6 +39,7 @@ inline int gemm_splits(const GemmPass &p, int64_t tiles, int min_stages) {
 inline bool gemm_split_ws(const GemmPass &p, int splits, hipStream_t s, GemmArgs &a) {
     a.part = nullptr;
     a.splits = 1;
+    a.slice0 = 0;
     if (splits <= 1) return false;
     void *ws = nullptr;
     if (split_workspace(s, (size_t)splits * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
@@ -109,6 +110,31 @@ hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && a.part) e = launch_split_reduce(p, a.part, a.splits, s);
     return e;
+}
+
+// One component of a pass alone (fused-stage kernel, ONLY = 1 or 2) into
+// slice `slice` of the fp32 partial sums `part`.
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY>
+hipError_t launch_component(const GemmPass &p, float *part, int slice, hipStream_t s) {
+    using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
+    GemmArgs a;
+    if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 4 >= ((int64_t)1 << 31) ||
+        2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
+        return hipErrorNotSupported;
+    a.M = p.M; a.Kin = p.Kin; a.Nout = p.Nout; a.bk = p.bk; a.bn = p.bn; a.D = p.D;
+    a.in = static_cast<const uint16_t *>(p.in);
+    a.W1 = static_cast<const uint16_t *>(p.W1);
+    a.W2 = static_cast<const uint16_t *>(p.W2);
+    a.bias = nullptr; a.h_in = nullptr; a.out = nullptr; a.h_out = nullptr;
+    a.epilogue = kEpiBias;
+    const int64_t tiles_m = (p.M + BM - 1) / BM;
+    const int64_t tiles_n = p.Nout / BN;
+    if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    a.tiles_n = (int)tiles_n;
+    a.tiles_total = (int)(tiles_m * tiles_n);
+    a.part = part; a.splits = 1; a.slice0 = slice;
+    dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, ONLY><<<a.tiles_total, C::kThreads, 0, s>>>(a);
+    return hipGetLastError();
 }
 
 // Whether a fused-stage tile fits (LDS of Gemm2Cfg, without instantiating it).
@@ -231,6 +257,32 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
         if (p.bn % 128 == 0) return launch_tile<BM, 128, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
     if constexpr (!OUT_T || 64 / D >= 16)
         if (p.bn % 64 == 0) return launch_tile<BM, 64, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
+    // An output transpose whose blocks are too narrow for any tile above
+    // (n_dyad 16 with blocks of 64 or 128 columns): the components run apart.
+    // Component 1 is a plain per-block GEMM on 64-column tiles; component 2
+    // alone tiles the transposed columns 256 at a time across blocks.  Their
+    // fp32 sums go to two slices that the split reduction adds in order.
+    if constexpr (OUT_T && D >= 8) {
+        constexpr bool k64 = tile2_ok<64, 256, 2, 4, D, IN_T, true, W_T>();
+        constexpr bool k32 = tile2_ok<32, 256, 1, 8, D, IN_T, true, W_T>();
+        if constexpr (k64 || k32) {
+            if (p.bn % 64 == 0 && p.Nout % 256 == 0) {
+                void *ws = nullptr;
+                if (split_workspace(s, 2 * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
+                    (void)hipGetLastError();
+                    return hipErrorNotSupported;
+                }
+                float *part = static_cast<float *>(ws);
+                hipError_t e = launch_component<128, 64, 2, 2, D, IN_T, false, W_T, 1>(p, part, 0, s);
+                if (e == hipSuccess) {
+                    if constexpr (k64) e = launch_component<64, 256, 2, 4, D, IN_T, true, W_T, 2>(p, part, 1, s);
+                    else e = launch_component<32, 256, 1, 8, D, IN_T, true, W_T, 2>(p, part, 1, s);
+                }
+                if (e == hipSuccess) e = launch_split_reduce(p, part, 2, s);
+                return e;
+            }
+        }
+    }
     return hipErrorNotSupported;
 }
 

@@ -31,6 +31,9 @@ SMALL = [  # (n_in, n_out, n_dyad, M)
     (256, 256, 1, 100),
     (1024, 1024, 8, 129),
     (4096, 4096, 16, 70),
+    (1024, 4096, 16, 100),  # input gradient under an output transpose, 64-column blocks:
+    (4096, 1024, 16, 100),  #   components apart; the same for the forward pass
+    (512, 1024, 8, 90),
     (192, 96, 3, 50),     # odd n_dyad, block widths 64 and 32
     (40, 24, 8, 33),      # block widths 5 and 3
 ]
