@@ -17,6 +17,7 @@ struct GemmArgs {
     float *part;        // split reduction: fp32 partial sums [slices][M][Nout], else null
     int splits;         // workgroups along the reduction per tile
     int slice0;         // partial slice of split 0
+    int unperm;         // partial sums of column j*D + g belong to column g*bn + j
 };
 
 // Epilogue of a BM x BN tile whose accumulators sit in the MFMA layout (wave w
@@ -116,6 +117,17 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
             if constexpr (PARTIAL) {
                 const __amdgpu_buffer_rsrc_t rP =
                     buffer_rsrc(a.part + ((int64_t)(a.slice0 + split) * a.M + m0) * a.Nout, 2u * o_bytes);
+                if (a.unperm) {
+                    // column c = j*D + g of the tile's output space is column g*bn + j
+                    const uint32_t rowb = 2u * vo - (uint32_t)(n0 + c8) * 4u;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int c = n0 + c8 + e;
+                        const uint32_t real = (uint32_t)((c % (int)a.D) * (int)a.bn + c / (int)a.D);
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x[e]), rP, (int)(rowb + 4u * real), 0, 0);
+                    }
+                    continue;
+                }
                 const u32x4_t lo = {__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])};
                 const u32x4_t hi = {__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]), __float_as_uint(x[7])};
                 __builtin_amdgcn_raw_buffer_store_b128(lo, rP, (int)(2u * vo), 0, 0);

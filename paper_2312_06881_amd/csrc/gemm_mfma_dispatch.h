@@ -40,6 +40,7 @@ inline bool gemm_split_ws(const GemmPass &p, int splits, hipStream_t s, GemmArgs
     a.part = nullptr;
     a.splits = 1;
     a.slice0 = 0;
+    a.unperm = 0;
     if (splits <= 1) return false;
     void *ws = nullptr;
     if (split_workspace(s, (size_t)splits * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
@@ -115,7 +116,7 @@ hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
 // One component of a pass alone (fused-stage kernel, ONLY = 1 or 2) into
 // slice `slice` of the fp32 partial sums `part`.
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY>
-hipError_t launch_component(const GemmPass &p, float *part, int slice, hipStream_t s) {
+hipError_t launch_component(const GemmPass &p, float *part, int slice, bool unperm, hipStream_t s) {
     using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
     GemmArgs a;
     if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 4 >= ((int64_t)1 << 31) ||
@@ -132,7 +133,7 @@ hipError_t launch_component(const GemmPass &p, float *part, int slice, hipStream
     if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     a.tiles_n = (int)tiles_n;
     a.tiles_total = (int)(tiles_m * tiles_n);
-    a.part = part; a.splits = 1; a.slice0 = slice;
+    a.part = part; a.splits = 1; a.slice0 = slice; a.unperm = unperm;
     dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, ONLY><<<a.tiles_total, C::kThreads, 0, s>>>(a);
     return hipGetLastError();
 }
@@ -173,6 +174,40 @@ constexpr int gemm_lds(int BM, int BN, int WGM, int D, bool OUT_T) {
 template <int BM, int BN, int WGM, int D, bool OUT_T>
 constexpr bool tile_ok() {
     return (!OUT_T || (BN % D == 0 && (BN / D) % 16 == 0)) && gemm_lds(BM, BN, WGM, D, OUT_T) <= 160 * 1024;
+}
+
+// The two components apart, for blocks too narrow for a tile (n_dyad 8 / 16
+// with blocks of 64 or 128 columns).  Component 1 is a plain per-block GEMM on
+// 64-column tiles.  Component 2 runs on the tiles of an output transpose,
+// 256 columns j*D + g at a time across blocks, which use every residue of an
+// input span; without an output transpose its sums are stored back at column
+// g*bn + j.  Both write fp32 slices that the split reduction adds in order.
+template <int D, bool IN_T, bool OUT_T, bool W_T>
+hipError_t launch_components(const GemmPass &p, hipStream_t s) {
+    if constexpr (D < 8) {
+        return hipErrorNotSupported;
+    } else {
+        constexpr bool k64 = tile2_ok<64, 256, 2, 4, D, IN_T, true, W_T>();
+        constexpr bool k32 = tile2_ok<32, 256, 1, 8, D, IN_T, true, W_T>();
+        if constexpr (!k64 && !k32) {
+            return hipErrorNotSupported;
+        } else {
+            if (p.bn % 64 != 0 || p.Nout % 256 != 0) return hipErrorNotSupported;
+            void *ws = nullptr;
+            if (split_workspace(s, 2 * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
+                (void)hipGetLastError();
+                return hipErrorNotSupported;
+            }
+            float *part = static_cast<float *>(ws);
+            hipError_t e = launch_component<128, 64, 2, 2, D, IN_T, false, W_T, 1>(p, part, 0, false, s);
+            if (e == hipSuccess) {
+                if constexpr (k64) e = launch_component<64, 256, 2, 4, D, IN_T, true, W_T, 2>(p, part, 1, !OUT_T, s);
+                else e = launch_component<32, 256, 1, 8, D, IN_T, true, W_T, 2>(p, part, 1, !OUT_T, s);
+            }
+            if (e == hipSuccess) e = launch_split_reduce(p, part, 2, s);
+            return e;
+        }
+    }
 }
 
 template <int D, bool IN_T, bool OUT_T, bool W_T>
@@ -245,6 +280,13 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
         if constexpr (tile2_ok<32, 256, 1, 8, D, IN_T, OUT_T, W_T>())
             if (p.bn % 256 == 0) return launch_tile2<32, 256, 1, 8, D, IN_T, OUT_T, W_T>(p, s);
     }
+    // An input transpose with narrow blocks: a tile inside one block would use
+    // one residue of every span it loads
+    if constexpr (IN_T && !OUT_T && D >= 8)
+        if (p.bn < 256) {
+            const hipError_t e = launch_components<D, IN_T, OUT_T, W_T>(p, s);
+            if (e != hipErrorNotSupported) return e;
+        }
     constexpr int BM = D >= 8 ? 64 : 128;
     // with an output transpose a 128 x 256 tile's D slabs need one workgroup per
     // CU; 64 x 256 keeps two, which measures faster
@@ -259,30 +301,7 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
         if (p.bn % 64 == 0) return launch_tile<BM, 64, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
     // An output transpose whose blocks are too narrow for any tile above
     // (n_dyad 16 with blocks of 64 or 128 columns): the components run apart.
-    // Component 1 is a plain per-block GEMM on 64-column tiles; component 2
-    // alone tiles the transposed columns 256 at a time across blocks.  Their
-    // fp32 sums go to two slices that the split reduction adds in order.
-    if constexpr (OUT_T && D >= 8) {
-        constexpr bool k64 = tile2_ok<64, 256, 2, 4, D, IN_T, true, W_T>();
-        constexpr bool k32 = tile2_ok<32, 256, 1, 8, D, IN_T, true, W_T>();
-        if constexpr (k64 || k32) {
-            if (p.bn % 64 == 0 && p.Nout % 256 == 0) {
-                void *ws = nullptr;
-                if (split_workspace(s, 2 * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
-                    (void)hipGetLastError();
-                    return hipErrorNotSupported;
-                }
-                float *part = static_cast<float *>(ws);
-                hipError_t e = launch_component<128, 64, 2, 2, D, IN_T, false, W_T, 1>(p, part, 0, s);
-                if (e == hipSuccess) {
-                    if constexpr (k64) e = launch_component<64, 256, 2, 4, D, IN_T, true, W_T, 2>(p, part, 1, s);
-                    else e = launch_component<32, 256, 1, 8, D, IN_T, true, W_T, 2>(p, part, 1, s);
-                }
-                if (e == hipSuccess) e = launch_split_reduce(p, part, 2, s);
-                return e;
-            }
-        }
-    }
+    if constexpr (OUT_T) return launch_components<D, IN_T, OUT_T, W_T>(p, s);
     return hipErrorNotSupported;
 }
 
