@@ -35,11 +35,12 @@ namespace dyad {
 namespace {
 
 constexpr int kSkWaves = 8;     // waves per workgroup
-constexpr int kSkMaxTok = 32;
+constexpr int kSkMaxTok = 256;
 
-// One component of a pass.  A workgroup's 8 waves are kw along the reduction
-// (each wave KR deep) times 8 / kw along the rows; each wave owns one row unit
-// of 128 output columns (8 MFMA tiles).
+// One component of a pass.  A workgroup's 8 waves are tw along the tokens
+// times kw along the reduction (each wave chunks x KR deep) times
+// 8 / (tw kw) along the rows; each wave owns one row unit of 128 output
+// columns (8 MFMA tiles) and 16 or 32 tokens.
 struct SkComp {
     const uint16_t *W;   // [D][bn][bk], or [D][bk][bn] when the pass reads weights transposed
     int gather;          // input column k*D + b (else b*bk + k)
@@ -55,6 +56,8 @@ struct SkArgs {
     float *part;         // [slices][M][Nout] fp32 partial sums
     int M, Kin, Nout, bk, bn, D;
     int row_units;       // row units per block
+    int tw;              // waves along the tokens in a workgroup (16 * MT tokens each)
+    int chunks;          // KR-deep chunks per wave
     SkComp c[2];
 };
 
@@ -77,17 +80,18 @@ template <bool W_T> struct SkShape {
 template <int MT, bool W_T>
 constexpr int sk_lds_bytes() { return (kSkWaves - 1) * SkShape<W_T>::NA * MT * 64 * 16; }
 
-// One wave: every load of its reduction range issued up front (the token
-// panel, then the weights), then the multiplies, then a fixed-order sum over
-// the workgroup's waves along k, and the partial sums stored.
-template <int MT, bool W_T, bool GATHER, int KR>
+// One wave: for each KR-deep chunk of its reduction range, every load issued
+// up front (the token panel, then the weights) and then the multiplies; after
+// the last chunk a fixed-order sum over the workgroup's waves along k, and the
+// partial sums stored.
+template <int MT, bool W_T, bool GATHER, int KR, bool LOOP>
 __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, int bid, unsigned char *lds) {
     constexpr int STEPS = KR / 32;
     constexpr int NA = SkShape<W_T>::NA, RU = SkShape<W_T>::RU;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, lg = lane >> 4;
-    const int kw_n = c.kw, rw_n = kSkWaves / kw_n;
-    const int wk = wave % kw_n, wr = wave / kw_n;
+    const int tw_n = a.tw, kw_n = c.kw, rw_n = kSkWaves / (kw_n * tw_n);
+    const int wt = wave % tw_n, wk = (wave / tw_n) % kw_n, wr = wave / (tw_n * kw_n);
     const int rg = bid % c.row_groups;
     bid /= c.row_groups;
     const int blk = bid % a.D;
@@ -96,80 +100,90 @@ __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, in
     const bool live = ru < a.row_units;
     ru = live ? ru : a.row_units - 1;                 // idle waves re-read a valid unit
     const int j0 = ru * RU;
-    const int k0 = (split * kw_n + wk) * KR;          // reduction range [k0, k0 + KR)
+    const int t0 = wt * 16 * MT;                      // the wave's first token
+    const int kspan = a.chunks * KR;                  // the wave's reduction range
+    const int kw0 = (split * kw_n + wk) * kspan;
     const int bk = a.bk, bn = a.bn, Kin = a.Kin, D = a.D;
 
-    const __amdgpu_buffer_rsrc_t rin = buffer_rsrc(a.in, (uint32_t)a.M * (uint32_t)Kin * 2u);
+    const int tok_left = a.M - t0;                    // tokens past the batch read zero
+    const __amdgpu_buffer_rsrc_t rin =
+        buffer_rsrc(a.in + (int64_t)t0 * Kin, tok_left > 0 ? (uint32_t)tok_left * (uint32_t)Kin * 2u : 0u);
     const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(c.W, (uint32_t)D * (uint32_t)bn * (uint32_t)bk * 2u);
-
-    // B operands: token 16 m + lr, k = k0 + 32 s + 8 lg ..+7 (zero past the batch)
-    uint4 xin[STEPS][MT];
-    uint32_t xg[STEPS][MT][8];
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s)
-#pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            const uint32_t row = (uint32_t)(16 * m + lr) * (uint32_t)Kin;
-            const int k = k0 + 32 * s + 8 * lg;
-            if constexpr (GATHER) {
-#pragma unroll
-                for (int t = 0; t < 8; ++t) xg[s][m][t] = ld_b16(rin, (row + (uint32_t)((k + t) * D + blk)) * 2u);
-            } else {
-                xin[s][m] = bload16(rin, (row + (uint32_t)(blk * bk + k)) * 2u, 0);
-            }
-        }
-    // A operands
-    uint4 w[STEPS][NA];
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s)
-#pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            uint32_t off;
-            if constexpr (W_T)   // row k0 + 32 s + 8 lg + i, columns j0 + 8 lr ..+7
-                off = ((uint32_t)(blk * bk + k0 + 32 * s + 8 * lg + i) * (uint32_t)bn + (uint32_t)(j0 + 8 * lr)) * 2u;
-            else                 // row j0 + 16 i + lr, k = k0 + 32 s + 8 lg ..+7
-                off = ((uint32_t)(blk * bn + j0 + 16 * i + lr) * (uint32_t)bk + (uint32_t)(k0 + 32 * s + 8 * lg)) * 2u;
-            w[s][i] = bload16(rw, off, 0);
-        }
-
-    // keep every load above the multiplies: the scheduler would otherwise sink
-    // them next to their use and leave one step of the stream in flight
-    __builtin_amdgcn_sched_barrier(0);
 
     f32x4_t acc[NA][MT];
 #pragma unroll
     for (int i = 0; i < NA; ++i)
 #pragma unroll
         for (int m = 0; m < MT; ++m) acc[i][m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const int nch = LOOP ? a.chunks : 1;   // one chunk: straight-line code
+    for (int ch = 0; ch < nch; ++ch) {
+        const int k0 = kw0 + ch * KR;
+        // B operands: token t0 + 16 m + lr, k = k0 + 32 s + 8 lg ..+7
+        uint4 xin[STEPS][MT];
+        uint32_t xg[STEPS][MT][8];
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-        bf16x8_t bf[MT];
+        for (int s = 0; s < STEPS; ++s)
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            if constexpr (GATHER) {
-                const uint4 v = make_uint4(xg[s][m][0] | (xg[s][m][1] << 16), xg[s][m][2] | (xg[s][m][3] << 16),
-                                           xg[s][m][4] | (xg[s][m][5] << 16), xg[s][m][6] | (xg[s][m][7] << 16));
-                bf[m] = as_frag(v);
-            } else {
-                bf[m] = as_frag(xin[s][m]);
+            for (int m = 0; m < MT; ++m) {
+                const uint32_t row = (uint32_t)(16 * m + lr) * (uint32_t)Kin;
+                const int k = k0 + 32 * s + 8 * lg;
+                if constexpr (GATHER) {
+#pragma unroll
+                    for (int t = 0; t < 8; ++t) xg[s][m][t] = ld_b16(rin, (row + (uint32_t)((k + t) * D + blk)) * 2u);
+                } else {
+                    xin[s][m] = bload16(rin, (row + (uint32_t)(blk * bk + k)) * 2u, 0);
+                }
+            }
+        // A operands
+        uint4 w[STEPS][NA];
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s)
+#pragma unroll
+            for (int i = 0; i < NA; ++i) {
+                uint32_t off;
+                if constexpr (W_T)   // row k0 + 32 s + 8 lg + i, columns j0 + 8 lr ..+7
+                    off = ((uint32_t)(blk * bk + k0 + 32 * s + 8 * lg + i) * (uint32_t)bn + (uint32_t)(j0 + 8 * lr)) * 2u;
+                else                 // row j0 + 16 i + lr, k = k0 + 32 s + 8 lg ..+7
+                    off = ((uint32_t)(blk * bn + j0 + 16 * i + lr) * (uint32_t)bk + (uint32_t)(k0 + 32 * s + 8 * lg)) * 2u;
+                w[s][i] = bload16(rw, off, 0);
+            }
+
+        // keep every load above the multiplies: the scheduler would otherwise
+        // sink them next to their use and leave one step of the stream in flight
+        __builtin_amdgcn_sched_barrier(0);
+
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+            bf16x8_t bf[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                if constexpr (GATHER) {
+                    const uint4 v = make_uint4(xg[s][m][0] | (xg[s][m][1] << 16), xg[s][m][2] | (xg[s][m][3] << 16),
+                                               xg[s][m][4] | (xg[s][m][5] << 16), xg[s][m][6] | (xg[s][m][7] << 16));
+                    bf[m] = as_frag(v);
+                } else {
+                    bf[m] = as_frag(xin[s][m]);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < NA; ++i) {
+                bf16x8_t af;
+                if constexpr (W_T) af = as_frag(column_of(w[s], i));   // tile i: columns j0 + 8 r + i
+                else af = as_frag(w[s][i]);
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+                    acc[i][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[m], acc[i][m], 0, 0, 0);
             }
         }
-#pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            bf16x8_t af;
-            if constexpr (W_T) af = as_frag(column_of(w[s], i));   // tile i: columns j0 + 8 r + i
-            else af = as_frag(w[s][i]);
-#pragma unroll
-            for (int m = 0; m < MT; ++m)
-                acc[i][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[m], acc[i][m], 0, 0, 0);
-        }
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // waves k-split inside the workgroup: waves 1.. hand over, wave 0 adds in order
     if (kw_n > 1) {
         f32x4_t *slot = reinterpret_cast<f32x4_t *>(lds);
         if (wk > 0) {
-            f32x4_t *mine = slot + ((wk - 1) * rw_n + wr) * NA * MT * 64;
+            f32x4_t *mine = slot + (((wk - 1) * rw_n + wr) * tw_n + wt) * NA * MT * 64;
 #pragma unroll
             for (int i = 0; i < NA; ++i)
 #pragma unroll
@@ -178,7 +192,7 @@ __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, in
         __syncthreads();
         if (wk > 0) return;
         for (int q = 1; q < kw_n; ++q) {
-            const f32x4_t *src = slot + ((q - 1) * rw_n + wr) * NA * MT * 64;
+            const f32x4_t *src = slot + (((q - 1) * rw_n + wr) * tw_n + wt) * NA * MT * 64;
 #pragma unroll
             for (int i = 0; i < NA; ++i)
 #pragma unroll
@@ -191,7 +205,7 @@ __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, in
     float *P = a.part + (int64_t)(c.slice0 + split) * a.M * a.Nout;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-        const int n = 16 * m + lr;
+        const int n = t0 + 16 * m + lr;
         if (n >= a.M) continue;
         float *row = P + (int64_t)n * a.Nout;
         if constexpr (!W_T) {
@@ -225,12 +239,13 @@ __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, in
 }
 
 // Both components in one launch: the first c[0].wgs workgroups run component 1.
-template <int MT, bool W_T, bool G2, int KR>
+// LOOP: waves take more than one chunk (batches above 32 tokens).
+template <int MT, bool W_T, bool G2, int KR, bool LOOP>
 __global__ void __launch_bounds__(64 * kSkWaves) skinny_part_kernel(SkArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char lds[sk_lds_bytes<MT, W_T>()];
     const int bid = blockIdx.x;
-    if (bid < a.c[0].wgs) skinny_wave<MT, W_T, false, KR>(a, a.c[0], bid, lds);
-    else skinny_wave<MT, W_T, G2, KR>(a, a.c[1], bid - a.c[0].wgs, lds);
+    if (bid < a.c[0].wgs) skinny_wave<MT, W_T, false, KR, LOOP>(a, a.c[0], bid, lds);
+    else skinny_wave<MT, W_T, G2, KR, LOOP>(a, a.c[1], bid - a.c[0].wgs, lds);
 }
 
 // out[n][f] = epilogue(sum of the slices, in slice order); 8 columns per thread.
@@ -289,40 +304,77 @@ __global__ void __launch_bounds__(256) skinny_reduce_kernel(GemmPass p, const fl
 
 // ---- host: plan, workspace, launch ------------------------------------------------
 
-// Reduction depth per wave: 128, i.e. 32 weight loads of 16 bytes per lane.
+// Reduction depth per wave and chunk: 128, i.e. 32 weight loads of 16 bytes
+// per lane; 64 for batches above 32 tokens, whose waves loop over chunks and
+// keep 32 tokens of accumulators.
 int sk_depth(const GemmPass &p) {
-    for (int kr = 128; kr >= 64; kr /= 2)
+    // (32 tokens of gathered transposed-weight operands also take 64: at 128
+    // they spill)
+    const bool deep = p.M <= 16 || (p.M <= 32 && !(p.w_t && p.in_t && p.D > 1));
+    for (int kr = deep ? 128 : 64; kr >= 64; kr /= 2)
         if (p.bk % kr == 0) return kr;
     return 0;
 }
 
-// kw (waves along k per workgroup) as large as the block allows, so that each
-// component leaves as few partial slices as possible, unless it idles more
-// than a quarter of the waves along the rows.
-bool plan_component(const GemmPass &p, int kr, SkComp &c, int row_units) {
-    const int kunits = (int)(p.bk / kr);
-    for (int kw = kSkWaves; kw >= 1; kw /= 2) {
-        if (kunits % kw != 0) continue;
-        const int rw = kSkWaves / kw;
-        const int groups = (row_units + rw - 1) / rw;
-        if (kw > 1 && 4 * (groups * rw - row_units) > groups * rw) continue;
-        c.kw = kw;
-        c.row_groups = groups;
-        c.wgs = (int)(p.D * groups * (kunits / kw));
-        return true;
-    }
-    return false;
-}
+// Workgroup shape and reduction split of a pass (both components alike).
+struct SkPlan {
+    int mt;              // 16-token MFMA column tiles per wave
+    int tw;              // waves along the tokens
+    int kw;              // waves along the reduction
+    int chunks;          // KR-deep chunks per wave
+    int row_groups;      // workgroups along the rows of one block
+    int splits;          // workgroups along the reduction of one block
+    int64_t wgs;         // workgroups per component
+};
 
-int sk_splits(const GemmPass &p, int kr, const SkComp &c) { return (int)(p.bk / kr) / c.kw; }
+// Tokens: 16 (at most 16) or 32 per wave, tw waves covering the batch.  kw as
+// large as the block allows, so each component leaves as few partial slices
+// as possible, unless it idles more than a quarter of the waves along the
+// rows.  Up to 32 tokens a wave takes one chunk, so all its loads are in flight
+// at once; with more tokens the weights take part in more multiply-adds, and
+// each wave takes as many chunks as still leave 128 workgroups per component.
+bool sk_plan(const GemmPass &p, int kr, SkPlan &pl) {
+    pl.mt = p.M <= 16 ? 1 : 2;
+    pl.tw = 1;
+    while (pl.tw * 16 * pl.mt < p.M) pl.tw *= 2;
+    if (pl.tw > kSkWaves) return false;
+    const int row_units = (int)(p.bn / 128);
+    const int kunits = (int)(p.bk / kr);
+    pl.kw = 1;
+    pl.row_groups = (row_units + kSkWaves / pl.tw - 1) / (kSkWaves / pl.tw);
+    for (int kw = kSkWaves / pl.tw; kw > 1; kw /= 2) {
+        if (kunits % kw != 0) continue;
+        const int rw = kSkWaves / (pl.tw * kw);
+        const int groups = (row_units + rw - 1) / rw;
+        if (4 * (groups * rw - row_units) > groups * rw) continue;
+        pl.kw = kw;
+        pl.row_groups = groups;
+        break;
+    }
+    const int per = kunits / pl.kw;
+    pl.chunks = 1;
+    if (pl.tw > 1)
+        for (int ch = per; ch > 1; --ch)
+            if (per % ch == 0 && p.D * pl.row_groups * (per / ch) >= 128) {
+                pl.chunks = ch;
+                break;
+            }
+    pl.splits = per / pl.chunks;
+    pl.wgs = p.D * pl.row_groups * pl.splits;
+    return pl.wgs < ((int64_t)1 << 30);
+}
 
 template <int MT, bool W_T, bool G2>
 hipError_t launch_part_kr(const SkArgs &a, int kr, hipStream_t s) {
     const dim3 grid((unsigned)(a.c[0].wgs + a.c[1].wgs)), block(64 * kSkWaves);
-    if (kr == 128) {
-        skinny_part_kernel<MT, W_T, G2, 128><<<grid, block, 0, s>>>(a);
+    if (a.chunks > 1) {
+        if (kr != 64) return hipErrorNotSupported;
+        skinny_part_kernel<MT, W_T, G2, 64, true><<<grid, block, 0, s>>>(a);
+    } else if (kr == 128) {
+        if constexpr (MT > 1 && W_T && G2) return hipErrorNotSupported;   // sk_depth gives 64
+        else skinny_part_kernel<MT, W_T, G2, 128, false><<<grid, block, 0, s>>>(a);
     } else if (kr == 64) {
-        skinny_part_kernel<MT, W_T, G2, 64><<<grid, block, 0, s>>>(a);
+        skinny_part_kernel<MT, W_T, G2, 64, false><<<grid, block, 0, s>>>(a);
     } else {
         return hipErrorNotSupported;
     }
@@ -413,33 +465,45 @@ hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices,
 
 bool skinny_ok(const GemmPass &p) {
     if (p.dtype != kBF16 || p.M < 1 || p.M > kSkMaxTok) return false;
+    // Above 32 tokens the waves of a workgroup split the batch and each reads
+    // the same weights, which pays only against the 32-token tiles the tiled
+    // kernels fall back to for an output transpose at n_dyad 16 with
+    // transposed weights (input gradients of IT / DT; measured at the wide
+    // layer with 256 tokens: 72-186 us against 171-220 us, while forward
+    // passes and other input gradients took 1.2-2.8x longer than tiled).
+    if (p.M > 32 && !(p.w_t && p.out_t && p.D >= 16)) return false;
     if (p.Kin != p.D * p.bk || p.Nout != p.D * p.bn) return false;
     // 32-bit buffer offsets: the weights and the input panel
     if (2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31) || 2 * p.M * p.Kin >= ((int64_t)1 << 31)) return false;
     if (p.bn % 128 != 0) return false;
     const int kr = sk_depth(p);
-    if (kr == 0) return false;
-    SkComp c{};
-    return plan_component(p, kr, c, (int)(p.bn / 128));
+    SkPlan pl;
+    return kr != 0 && sk_plan(p, kr, pl);
 }
 
 hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s) {
     if (!skinny_ok(p)) return hipErrorNotSupported;
     const int kr = sk_depth(p);
+    SkPlan pl;
+    sk_plan(p, kr, pl);
     SkArgs a{};
     a.in = static_cast<const uint16_t *>(p.in);
     a.M = (int)p.M; a.Kin = (int)p.Kin; a.Nout = (int)p.Nout;
     a.bk = (int)p.bk; a.bn = (int)p.bn; a.D = (int)p.D;
     a.row_units = (int)(p.bn / 128);
+    a.tw = pl.tw;
+    a.chunks = pl.chunks;
     int slices = 0;
     for (int c = 0; c < 2; ++c) {
         SkComp &k = a.c[c];
-        plan_component(p, kr, k, a.row_units);
         k.W = static_cast<const uint16_t *>(c == 0 ? p.W1 : p.W2);
         k.gather = c == 1 && p.in_t && p.D > 1;
         k.out_t = c == 1 && p.out_t;
+        k.kw = pl.kw;
+        k.row_groups = pl.row_groups;
+        k.wgs = (int)pl.wgs;
         k.slice0 = slices;
-        slices += sk_splits(p, kr, k);
+        slices += pl.splits;
     }
     const size_t bytes = (size_t)slices * (size_t)p.M * (size_t)p.Nout * sizeof(float);
     void *ws = nullptr;
@@ -449,7 +513,7 @@ hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s) {
     }
     a.part = static_cast<float *>(ws);
     const bool g2 = a.c[1].gather != 0;
-    hipError_t e = p.M <= 16 ? launch_part_mt<1>(a, kr, p.w_t, g2, s) : launch_part_mt<2>(a, kr, p.w_t, g2, s);
+    hipError_t e = pl.mt == 1 ? launch_part_mt<1>(a, kr, p.w_t, g2, s) : launch_part_mt<2>(a, kr, p.w_t, g2, s);
     if (e == hipSuccess) e = launch_split_reduce(p, a.part, slices, s);
     return e;
 }

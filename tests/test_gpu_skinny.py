@@ -1,4 +1,4 @@
-"""GPU parity of the small-batch paths (at most 32 tokens): forward, input
+"""GPU parity of the small-batch paths (up to 256 tokens): forward, input
 gradient and weight / bias gradients through the C-ABI against the CPU
 oracle, element by element.
 
@@ -99,6 +99,33 @@ def test_backward_dw_few_tokens(shape, variant, M):
     assert_close(dw1, r1, "bf16", "dW1")
     assert_close(dw2, r2, "bf16", "dW2")
     assert_close(db, rb, "bf16", "db")
+
+
+MID_SHAPES = [(512, 1024, 4), (768, 1536, 3), (1536, 512, 4), (2048, 8192, 16), (4096, 2048, 16)]
+MID_TOKENS = [33, 100, 256]
+
+
+@pytest.mark.parametrize("M", MID_TOKENS)
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("shape", MID_SHAPES, ids=case_id)
+def test_forward_and_dx_up_to_256_tokens(shape, variant, M):
+    """Batches of 33-256 tokens (GELU forward with stash, GELU' input gradient).
+    At n_dyad 16 the output-transposed input gradients take the small-batch
+    path, its waves splitting the tokens 32 at a time and looping over chunks
+    of the reduction; the other passes run on the tiled kernels."""
+    n_in, n_out, D = shape
+    banner("mid", shape, variant, M)
+    L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=M)
+    y, h = dy.forward(gpu(L.X), gpu(L.W1), gpu(L.W2), gpu(L.bias), variant=variant, act="gelu", stash_h=True)
+    dx = dy.backward_dx(gpu(L.dZ), gpu(L.W1), gpu(L.W2), variant=variant, act_in="gelu", h_in=gpu(L.H_in))
+    torch.cuda.synchronize()
+    ry, rh = oracle.forward(variant, n_in, n_out, D, L.f64("X"), L.f64("W1"), L.f64("W2"), L.f64("bias"),
+                            act=oracle.ACT_GELU, want_h=True)
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, L.f64("dZ"), L.f64("W1"), L.f64("W2"),
+                             act_in=oracle.ACT_GELU, H_in=L.f64("H_in"))
+    assert_close(y, ry, "bf16", "Y")
+    assert_close(h, rh, "bf16", "H")
+    assert_close(dx, rdx, "bf16", "dX")
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
