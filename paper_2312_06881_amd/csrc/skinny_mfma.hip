@@ -88,10 +88,13 @@ template <int MT, bool W_T, bool GATHER, int KR, bool LOOP>
 __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, int bid, unsigned char *lds) {
     constexpr int STEPS = KR / 32;
     constexpr int NA = SkShape<W_T>::NA, RU = SkShape<W_T>::RU;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar arithmetic
     const int lr = lane & 15, lg = lane >> 4;
-    const int tw_n = a.tw, kw_n = c.kw, rw_n = kSkWaves / (kw_n * tw_n);
-    const int wt = wave % tw_n, wk = (wave / tw_n) % kw_n, wr = wave / (tw_n * kw_n);
+    // tw and kw are powers of two: the wave's place by shifts, before any load
+    const int tw_n = a.tw, kw_n = c.kw, tw_l = __builtin_ctz(tw_n), kw_l = __builtin_ctz(kw_n);
+    const int rw_n = kSkWaves >> (tw_l + kw_l);
+    const int wt = wave & (tw_n - 1), wk = (wave >> tw_l) & (kw_n - 1), wr = wave >> (tw_l + kw_l);
     const int rg = bid % c.row_groups;
     bid /= c.row_groups;
     const int blk = bid % a.D;
@@ -176,7 +179,7 @@ __device__ __forceinline__ void skinny_wave(const SkArgs &a, const SkComp &c, in
                     acc[i][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[m], acc[i][m], 0, 0, 0);
             }
         }
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (LOOP) __builtin_amdgcn_sched_barrier(0);   // the next chunk's loads stay below
     }
 
     // waves k-split inside the workgroup: waves 1.. hand over, wave 0 adds in order
