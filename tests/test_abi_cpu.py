@@ -114,3 +114,19 @@ def test_backward_dw_rejects_and_workspace_size():
         w5 = dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, dtype)
         assert w5 > 0 and w5 % per_split == 0
     assert dy.dyad_dw_workspace_bytes(9, 768, 3072, 4, 16384, 1) == 0
+
+
+def test_dw_workspace_single_split():
+    """A batch that one token split covers needs no workspace (the tiles store
+    bf16 results directly); a long batch on a narrow layer splits the tokens
+    and needs fp32 partials of dW1, dW2 and db for every split."""
+    for M in (1, 16, 32):
+        for v in (0, 1, 2):
+            assert dy.dyad_dw_workspace_bytes(v, 8192, 32768, 16, M, 1) == 0
+    per_split = 4 * (2 * 768 * 3072 // 4 + 3072)
+    need = dy.dyad_dw_workspace_bytes(0, 768, 3072, 4, 16384, 1)
+    assert need > 0 and need % per_split == 0 and need // per_split >= 2
+    # and a call without one is then refused before any launch
+    a = dict(variant=0, n_in=768, n_out=3072, n_dyad=4, M=16384, dtype=1, dZ=FAKE, X=FAKE,
+             dW1=FAKE, dW2=FAKE, dbias=None, workspace=None, workspace_bytes=0, stream=None)
+    assert dy.dyad_backward_dw(**a) == -5
