@@ -208,8 +208,8 @@ def main():
         summarize_pmc(args, *args.summarize_pmc)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(the multi-GPU design is described, not built)",
+        print(json.dumps({"error": "libdyad runs on one GPU; --gpus must be 1 "
+                                   "(token sharding over several GPUs is a design, not code)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     if args.block:

@@ -1,5 +1,5 @@
-"""The benchmark's command-line contract: one JSON line with the fields the
-driver reads, and a refusal of more than one GPU (this build runs on one)."""
+"""The benchmark's command-line contract: one JSON line with the fields a
+harness reads, and a refusal of more than one GPU (libdyad runs on one)."""
 import json
 import os
 import subprocess
