@@ -158,3 +158,31 @@ def test_wide_few_tokens_all_passes(variant):
     assert_close(y, ry, "bf16", "Y")
     assert_close(dx, rdx, "bf16", "dX")
     assert np.isfinite(y.float().cpu().numpy()).all()
+
+
+def test_two_streams_keep_their_workspaces():
+    """Split sums live in one workspace per stream: passes queued on two
+    streams at once give bitwise the results of the same passes run one after
+    the other."""
+    banner("two_streams")
+    n_in, n_out, D, M = 8192, 32768, 16, 16
+    La = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=1)
+    Lb = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=2)
+    a = [gpu(t) for t in (La.X, La.W1, La.W2, La.bias, La.dZ)]
+    b = [gpu(t) for t in (Lb.X, Lb.W1, Lb.W2, Lb.bias, Lb.dZ)]
+    ref = []
+    for X, W1, W2, bias, dZ in (a, b):
+        ref.append((dy.forward(X, W1, W2, bias, variant="DT"), dy.backward_dx(dZ, W1, W2, variant="DT")))
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    got = []
+    for _ in range(3):
+        outs = []
+        for st, (X, W1, W2, bias, dZ) in ((s1, a), (s2, b)):
+            with torch.cuda.stream(st):
+                outs.append((dy.forward(X, W1, W2, bias, variant="DT"), dy.backward_dx(dZ, W1, W2, variant="DT")))
+        got.append(outs)
+    torch.cuda.synchronize()
+    for outs in got:
+        for (y, dx), (ry, rdx) in zip(outs, ref):
+            assert torch.equal(y, ry) and torch.equal(dx, rdx)
