@@ -74,9 +74,10 @@ hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t s);
 // 32 bits.
 hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t s);
 
-// Small-batch grouped GEMM (bf16, at most 32 tokens, widths that n_dyad
-// divides): the reduction split over workgroups, fp32 partial sums in a
-// stream-ordered workspace from a per-device pool, added in a fixed order.
+// Small-batch grouped GEMM (bf16, up to 32 tokens -- 256 for output-transposed
+// input gradients at n_dyad 16 --, widths that n_dyad divides into blocks of a
+// multiple of 128 columns): the reduction split over workgroups, fp32 partial
+// sums in the stream's split workspace, added in a fixed order.
 // hipErrorNotSupported (launching nothing) when skinny_ok() is false.
 bool skinny_ok(const GemmPass &p);
 hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s);

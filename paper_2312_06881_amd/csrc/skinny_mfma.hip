@@ -1,5 +1,6 @@
-// Small-batch grouped GEMM (bf16, at most 32 tokens) for the forward pass and
-// the input gradient: the regime where the weights are the traffic.
+// Small-batch grouped GEMM (bf16; up to 32 tokens, and up to 256 for the
+// output-transposed input gradients at n_dyad 16) for the forward pass and the
+// input gradient: the regime where the weights are the traffic.
 //
 // With few tokens each weight entry takes part in at most 32 multiply-adds, so
 // a pass is a stream of the two weight tensors from HBM and everything else is
@@ -14,8 +15,8 @@
 // bf16, so results do not depend on scheduling.
 //
 // Operands.  With so little work per weight byte, what matters is how much of
-// the stream is in flight: each wave issues every load of its reduction range
-// up front -- its 16-token panel (16-byte loads along k, or 2-byte loads of
+// the stream is in flight: each wave issues every load of a reduction chunk
+// up front -- its 16- or 32-token panel (16-byte loads along k, or 2-byte loads of
 // the residue k*D + b under an input transpose), then 32 16-byte weight loads
 // -- and multiplies once they land.  Untransposed [bn][bk] weight rows are
 // contiguous along k: one load per lane and 16-row tile gives its MFMA operand.
@@ -24,7 +25,8 @@
 // loads serve 8 tiles whose rows are the output columns j, j + 8, j + 16, ...
 // of a 128-column strip.  The 8 waves of a workgroup split the reduction of
 // their rows further and add their accumulators through LDS in wave order
-// before storing the partial sums.
+// before storing the partial sums; above 32 tokens they split the batch
+// instead, 32 tokens a wave, each looping over chunks of the reduction.
 #include <mutex>
 #include <vector>
 
