@@ -52,11 +52,13 @@ def test_linear_autograd(variant, dtype):
     assert_close(mod.bias.grad, rb, dtype, "db")
 
 
+@pytest.mark.parametrize("shape", [(256, 1024, 4, 130), (2048, 8192, 16, 16)], ids=["tiled", "16-tokens"])
 @pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
-def test_ff_autograd(variant):
-    """DyadFF (fc1 -> GELU -> fc2) forward and backward vs the oracle's layer chain."""
-    d, ffn, D, M = 256, 1024, 4, 130
-    banner("ff", variant)
+def test_ff_autograd(variant, shape):
+    """DyadFF (fc1 -> GELU -> fc2) forward and backward vs the oracle's layer chain;
+    the 16-token case runs every pass on the small-batch paths."""
+    d, ffn, D, M = shape
+    banner("ff", variant, shape)
     L1 = layer_inputs(d, ffn, D, M, "bf16")
     L2 = layer_inputs(ffn, d, D, M, "bf16", seed_offset=100)
     ff = DyadFF(d, ffn, D, variant, device=DEV)
