@@ -33,8 +33,8 @@
  * partial sums then go to a library-owned device buffer, one per (device,
  * stream), taken in stream order from a per-device memory pool of the current
  * device the first time that stream needs it, regrown in stream order when a
- * later call needs more, and kept until the process ends (at most a few
- * split slices of M x n_out fp32).  Calls on one stream share it in stream
+ * later call needs more, and kept until the process ends (a few slices of
+ * M x n_out fp32, at most 2 GiB).  Calls on one stream share it in stream
  * order; calls on different streams never share it.  When it cannot be had,
  * the call runs without the split.  Every call only enqueues work on `stream`
  * (NULL = the null stream) and returns without synchronising; results are

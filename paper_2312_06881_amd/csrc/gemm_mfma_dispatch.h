@@ -193,8 +193,11 @@ hipError_t launch_components(const GemmPass &p, hipStream_t s) {
             return hipErrorNotSupported;
         } else {
             if (p.bn % 64 != 0 || p.Nout % 256 != 0) return hipErrorNotSupported;
+            // the two fp32 slices stay with the stream: at most 2 GiB of them
+            const size_t bytes = 2 * (size_t)p.M * (size_t)p.Nout * sizeof(float);
+            if (bytes > ((size_t)2 << 30)) return hipErrorNotSupported;
             void *ws = nullptr;
-            if (split_workspace(s, 2 * (size_t)p.M * (size_t)p.Nout * sizeof(float), &ws) != hipSuccess) {
+            if (split_workspace(s, bytes, &ws) != hipSuccess) {
                 (void)hipGetLastError();
                 return hipErrorNotSupported;
             }
