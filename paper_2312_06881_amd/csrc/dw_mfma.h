@@ -48,6 +48,7 @@ namespace dyad {
 struct DwArgs {
     int64_t M, n_in, n_out, bi, bo;
     const uint16_t *dZ, *X;
+    const uint16_t *dZ2, *X2;   // component 2's operands (dZ / X, or block-ordered copies)
     float *part;          // [splits][2][D][bo][bi]
     float *part_db;       // [splits][n_out]
     uint16_t *dW1, *dW2, *db;
@@ -259,8 +260,8 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         const int64_t left = t_end - tok;
         const uint32_t rows = left <= 0 ? 0u : (uint32_t)(left < kStageK ? left : kStageK);
         const int64_t base = left <= 0 ? 0 : tok;
-        fetch_side(SA{}, sa, set, buffer_rsrc(a.dZ + base * a.n_out, rows * n_out * 2u), rows);
-        fetch_side(SB{}, sb, set, buffer_rsrc(a.X + base * a.n_in, rows * n_in * 2u), rows);
+        fetch_side(SA{}, sa, set, buffer_rsrc((C2 ? a.dZ2 : a.dZ) + base * a.n_out, rows * n_out * 2u), rows);
+        fetch_side(SB{}, sb, set, buffer_rsrc((C2 ? a.X2 : a.X) + base * a.n_in, rows * n_in * 2u), rows);
     };
     // ---- registers -> LDS stage buffer
     auto stash_side = [&](auto side, auto swz, auto &sl, auto set, unsigned char *buf) {
@@ -465,6 +466,8 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.M = p.M; a.n_in = p.n_in; a.n_out = p.n_out; a.bi = p.bi; a.bo = p.bo;
     a.dZ = static_cast<const uint16_t *>(p.dZ);
     a.X = static_cast<const uint16_t *>(p.X);
+    a.dZ2 = static_cast<const uint16_t *>(p.dZ2 ? p.dZ2 : p.dZ);
+    a.X2 = static_cast<const uint16_t *>(p.X2 ? p.X2 : p.X);
     a.direct = pl.splits == 1;
     a.part = a.direct ? nullptr : static_cast<float *>(p.ws);
     a.part_db = a.direct ? nullptr : a.part + (int64_t)pl.splits * 2 * p.D * p.bo * p.bi;
@@ -523,7 +526,9 @@ inline bool dw_mg_available(int D, int BJ, int BK, int WJN, int WKN) {
     return false;
 }
 
-// Per-variant launchers (one translation unit each).
+// Per-variant launchers (one translation unit each); launch_dw_plain: both
+// components on block-ordered operands (n_dyad 8 and 16).
+hipError_t launch_dw_plain(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_it(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_ot(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_dt(const DwPass &p, const DwPlan &pl, hipStream_t s);

@@ -82,22 +82,84 @@ bool choose(const DwPass &p, DwPlan &pl) {
     return false;
 }
 
+// Large batches at n_dyad 8 and 16 with a transpose: component 2's strided
+// operands (dZ columns j*D + g, X columns k*D + g) are de-interleaved once into
+// block-ordered copies in the stream's workspace (each at most 2 GiB), and
+// both components then run on the plain tiles, whose operand reads are whole
+// rows of one group instead of spans of all D.  Measured on gfx950 against
+// the fused tiles, this pays from 2048 tokens at n_dyad 16 (1.1-1.6x at
+// d = 1024, 3-4x on the wide layer 8192 -> 32768 at 32768 tokens) and from
+// 8192 at n_dyad 8 (at 2048 tokens it lost by up to 15%).
+bool dw_permuted(const DwPass &p) {
+    if ((p.D != 8 && p.D != 16) || (!p.in_t && !p.out_t)) return false;
+    if (p.M < (p.D == 16 ? 2048 : 8192)) return false;
+    if ((p.out_t && p.bo % 32 != 0) || (p.in_t && p.bi % 32 != 0)) return false;
+    const int64_t cap = (int64_t)1 << 31;
+    return !(p.out_t && p.M * p.n_out * 2 > cap) && !(p.in_t && p.M * p.n_in * 2 > cap);
+}
+
+// The plan a pass runs with (for the permuted form, that of plain operands).
+bool plan(const DwPass &p, DwPlan &pl, bool *permuted) {
+    *permuted = false;
+    if (dw_permuted(p)) {
+        DwPass q = p;
+        q.in_t = q.out_t = false;
+        if (choose(q, pl)) {
+            *permuted = true;
+            return true;
+        }
+    }
+    return choose(p, pl);
+}
+
 }  // namespace
 
 bool mfma_dw_ok(const DwPass &p) {
     DwPlan pl;
-    return choose(p, pl);
+    bool permuted;
+    return plan(p, pl, &permuted);
+}
+
+// Partial-sum bytes of plan pl (one split writes the results directly).
+static size_t plan_workspace(const DwPass &p, const DwPlan &pl) {
+    if (pl.splits == 1) return 0;
+    return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi + p.n_out) * sizeof(float);
 }
 
 size_t mfma_dw_workspace(const DwPass &p) {
     DwPlan pl;
-    if (!choose(p, pl) || pl.splits == 1) return 0;   // one split writes the results directly
-    return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi + p.n_out) * sizeof(float);
+    bool permuted;
+    return plan(p, pl, &permuted) ? plan_workspace(p, pl) : 0;
 }
 
 hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s) {
     DwPlan pl;
-    if (!choose(p, pl)) return hipErrorNotSupported;
+    bool permuted;
+    if (!plan(p, pl, &permuted)) return hipErrorNotSupported;
+    if (permuted) {
+        const size_t zb = p.out_t ? (size_t)p.M * (size_t)p.n_out * 2 : 0;
+        const size_t xb = p.in_t ? (size_t)p.M * (size_t)p.n_in * 2 : 0;
+        void *ws = nullptr;
+        hipError_t e = split_workspace(s, zb + xb, &ws);
+        if (e == hipSuccess) {
+            DwPass q = p;
+            q.in_t = q.out_t = false;
+            uint16_t *z2 = static_cast<uint16_t *>(ws), *x2 = z2 + zb / 2;
+            if (p.out_t) {
+                e = launch_deinterleave(static_cast<const uint16_t *>(p.dZ), z2, p.M, p.bo, (int)p.D, s);
+                q.dZ2 = z2;
+            }
+            if (e == hipSuccess && p.in_t) {
+                e = launch_deinterleave(static_cast<const uint16_t *>(p.X), x2, p.M, p.bi, (int)p.D, s);
+                q.X2 = x2;
+            }
+            return e == hipSuccess ? launch_dw_plain(q, pl, s) : e;
+        }
+        // no room for the copies: the fused form, if the caller's workspace
+        // (sized for the plan above) also holds that plan's partial sums
+        if (!choose(p, pl) || plan_workspace(p, pl) > p.ws_bytes) return e;
+        (void)hipGetLastError();
+    }
     if (p.in_t && !p.out_t) return launch_dw_it(p, pl, s);
     if (!p.in_t && p.out_t) return launch_dw_ot(p, pl, s);
     if (p.in_t && p.out_t) return launch_dw_dt(p, pl, s);

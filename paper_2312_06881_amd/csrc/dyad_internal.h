@@ -53,6 +53,9 @@ struct DwPass {
     void *dW1, *dW2, *db;
     void *ws;
     size_t ws_bytes;
+    // component 2's operands when they differ from dZ / X (block-ordered copies
+    // of them, read with in_t / out_t false); null: dZ / X
+    const void *dZ2, *X2;
 };
 
 // General kernels: any shape, any D, both dtypes (vector ALU, tiled).  The
@@ -85,9 +88,16 @@ hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s);
 // Split reductions of the grouped GEMM: a workspace of at least `bytes` for
 // stream s (one per device and stream, kept between calls and regrown in
 // stream order), and the kernel that adds `slices` fp32 partial sums
-// [slices][M][Nout] in slice order and applies the pass's epilogue.
+// [slices][M][Nout] in slice order and applies the pass's epilogue (with
+// perm_last, the last slice holds block-order sums: output column j*D + g at
+// column g*bn + j).
 hipError_t split_workspace(hipStream_t s, size_t bytes, void **out);
-hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s);
+hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s,
+                               bool perm_last = false);
+
+// out[n][g*bk + k] = in[n][k*D + g] for M token rows of D*bk bf16 values
+// (bk a multiple of 32, D a divisor of 64, 16-byte aligned rows).
+hipError_t launch_deinterleave(const uint16_t *in, uint16_t *out, int64_t M, int64_t bk, int D, hipStream_t s);
 
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
 // when the pass's shape has no matching tile configuration (zero-padded

@@ -27,7 +27,10 @@ struct GemmArgs {
 // output transpose).  smem needs 2 * kEpiElems floats and must be free.  With
 // a split reduction (a.part set) the tile's fp32 sums go to slice `split` of
 // the partial sums instead, in real column order and without the epilogue.
-template <class C, int BM, int BN, int D, bool OUT_T, bool PARTIAL>
+// ADD: before the epilogue each sum gets the fp32 value of slice a.slice0 of
+// a.part at its column, or with a.unperm at the block-order place of it
+// (column g*bn + j for column j*D + g).
+template <class C, int BM, int BN, int D, bool OUT_T, bool PARTIAL, bool ADD = false>
 __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned char *smem,
                                                  const f32x4_t (&acc)[C::kSubM][C::kSubN], int64_t m0, int n0,
                                                  int64_t rows_left, int tid, int lane, int wave, int wn0,
@@ -75,6 +78,9 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
         for (int q = 0; q < kBiasQ; ++q) bq[q] = ldg16(a.bias + n0 + c8of[q]);
     }
     uint4 hq[2][kQ];
+    float pa[ADD ? kQ : 1][8];
+    const __amdgpu_buffer_rsrc_t rS =
+        ADD ? buffer_rsrc(a.part + ((int64_t)a.slice0 * a.M + m0) * a.Nout, 2u * o_bytes) : rO;
     if (grad) {
 #pragma unroll
         for (int q = 0; q < kQ; ++q) hq[0][q] = bload16(rH, voE[q], 0);
@@ -83,6 +89,30 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
 #pragma unroll
     for (int i = 0; i < C::kSubM; ++i) {
         float *ldsE = reinterpret_cast<float *>(smem) + (i & 1) * C::kEpiElems;
+        if constexpr (ADD) {
+            // this block row's slice values, in flight over the LDS round trip
+#pragma unroll
+            for (int q = 0; q < kQ; ++q) {
+                const uint32_t vb = 2u * (voE[q] + (uint32_t)i * row16);
+                if (a.unperm) {
+                    const uint32_t rowb = vb - (uint32_t)(n0 + c8of[q]) * 4u;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int c = n0 + c8of[q] + e;
+                        const uint32_t at = (uint32_t)((c % (int)a.D) * (int)a.bn + c / (int)a.D);
+                        pa[q][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rS, (int)(rowb + 4u * at), 0, 0));
+                    }
+                } else {
+                    const u32x4_t lo = __builtin_amdgcn_raw_buffer_load_b128(rS, (int)vb, 0, 0);
+                    const u32x4_t hi = __builtin_amdgcn_raw_buffer_load_b128(rS, (int)(vb + 16u), 0, 0);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        pa[q][e] = __uint_as_float(lo[e]);
+                        pa[q][4 + e] = __uint_as_float(hi[e]);
+                    }
+                }
+            }
+        }
 #pragma unroll
         for (int j = 0; j < C::kSubN; ++j) {
             const int col = wn0 + j * 16 + (lane & 15);
@@ -133,6 +163,10 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
                 __builtin_amdgcn_raw_buffer_store_b128(lo, rP, (int)(2u * vo), 0, 0);
                 __builtin_amdgcn_raw_buffer_store_b128(hi, rP, (int)(2u * vo + 16u), 0, 0);
                 continue;
+            }
+            if constexpr (ADD) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += pa[q][e];
             }
             if (grad) {
                 const uint4 h = hq[i & 1][q];

@@ -66,7 +66,9 @@ struct Gemm2Cfg {
 };
 
 // ONLY = 1 or 2: that component alone, into fp32 partial sums (a.part, slice
-// a.slice0).  Component 2 alone under an output transpose needs no output
+// a.slice0).  ONLY = 3: component 1 alone with the full epilogue, its sums
+// first added to those of slice a.slice0 (read at the block-order place of
+// each column when a.unperm).  Component 2 alone under an output transpose needs no output
 // block per tile: its columns f = j*D + g take weight group f % D and row
 // f / D whatever block f falls in.
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY = 0>
@@ -187,7 +189,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             for (int q = 0; q < C::kQA1; ++q) ra1[q] = bload16(rA, voA1[q], kk * 2u);
         }
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQA2); ++q) {
+        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQA2); ++q) {
             if constexpr (IN_T) {
 #pragma unroll
                 for (int d = 0; d < D; ++d) ra2[q][d] = bload16(rA, voA2[q] + d * 16u, kk * D * 2u);
@@ -201,7 +203,7 @@ dyad_gemm_mfma2(GemmArgs a) {
 #pragma unroll
             for (int d = 0; d < C::kVB1; ++d) rb1[q][d] = bload16(rW1, voB1[q] + d * 16u, kb);
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQB); ++q) rb2[q] = bload16(rW2, voB2[q], kb);
+        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQB); ++q) rb2[q] = bload16(rW2, voB2[q], kb);
     };
 
     // ---- registers -> LDS stage buffer
@@ -210,7 +212,7 @@ dyad_gemm_mfma2(GemmArgs a) {
         for (int q = 0; q < (ONLY == 2 ? 0 : C::kQA1); ++q)
             if (C::kRowChunks % T == 0 || okA1[q]) *reinterpret_cast<uint4 *>(buf + loA1[q]) = ra1[q];
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQA2); ++q) {
+        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQA2); ++q) {
             if (C::kUnitsA2 % T != 0 && !okA2[q]) continue;
             if constexpr (IN_T) {
                 uint4 span[D];
@@ -238,7 +240,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             }
         }
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 ? 0 : C::kQB); ++q)
+        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQB); ++q)
             if (C::kUnitsB % T == 0 || okB2[q]) *reinterpret_cast<uint4 *>(buf + loB2[q]) = rb2[q];
     };
 
@@ -266,7 +268,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             }
         }
 #pragma unroll
-        for (int rr = 0; rr < (ONLY == 1 ? 0 : C::kRPW); ++rr) {
+        for (int rr = 0; rr < (ONLY == 1 || ONLY == 3 ? 0 : C::kRPW); ++rr) {
             const int r = OUT_T ? (wn0 + rr * C::kCPR) / C::kCPR : 0;
             const unsigned char *slab = buf + C::kOffA2 + r * C::kSlab;
 #pragma unroll
@@ -310,7 +312,11 @@ dyad_gemm_mfma2(GemmArgs a) {
         __syncthreads();
     }
 
-    gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
+    if constexpr (ONLY == 3)
+        gemm_epilogue_as<C, BM, BN, D, OUT_T, false, true>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0,
+                                                           split);
+    else
+        gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
 }
 
 }  // namespace dyad

@@ -6,6 +6,17 @@
 
 namespace dyad {
 
+// Whether a pass at n_dyad 8 / 16 with a transpose takes launch_permuted
+// (measured on gfx950 against the fused tiles at 2048 and 16384 tokens: at
+// n_dyad 16 it wins from reduction blocks of 128 with an output transpose and
+// from 256 without, and for the input gradient under an output transpose
+// from blocks of 64 once the batch is large; at n_dyad 8 from blocks of 512).
+inline bool permuted_pays(int D, bool out_t, bool w_t, int64_t M, int64_t bk) {
+    if (M < 2048) return false;
+    if (D >= 16) return bk >= (out_t ? 128 : 256) || (w_t && out_t && M >= 8192 && bk >= 64);
+    return bk >= 512;
+}
+
 // Workgroups per CU: two 4-wave workgroups when both the tile's LDS and its
 // registers fit twice (two caps a wave at 256 VGPRs, so accumulators above 128
 // per lane need one); an 8-wave workgroup runs alone.
@@ -114,7 +125,9 @@ hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
 }
 
 // One component of a pass alone (fused-stage kernel, ONLY = 1 or 2) into
-// slice `slice` of the fp32 partial sums `part`.
+// slice `slice` of the fp32 partial sums `part`; with ONLY = 3, component 1
+// into the pass's output with its epilogue, adding that slice (at the
+// block-order place of each column with `unperm`).
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY>
 hipError_t launch_component(const GemmPass &p, float *part, int slice, bool unperm, hipStream_t s) {
     using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
@@ -128,6 +141,13 @@ hipError_t launch_component(const GemmPass &p, float *part, int slice, bool unpe
     a.W2 = static_cast<const uint16_t *>(p.W2);
     a.bias = nullptr; a.h_in = nullptr; a.out = nullptr; a.h_out = nullptr;
     a.epilogue = kEpiBias;
+    if constexpr (ONLY == 3) {
+        a.bias = static_cast<const uint16_t *>(p.bias);
+        a.h_in = static_cast<const uint16_t *>(p.h_in);
+        a.out = static_cast<uint16_t *>(p.out);
+        a.h_out = static_cast<uint16_t *>(p.h_out);
+        a.epilogue = p.epilogue;
+    }
     const int64_t tiles_m = (p.M + BM - 1) / BM;
     const int64_t tiles_n = p.Nout / BN;
     if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
@@ -213,10 +233,76 @@ hipError_t launch_components(const GemmPass &p, hipStream_t s) {
     }
 }
 
+// Large batches at n_dyad 8 and 16 with a transpose.  A fused tile under an
+// output transpose holds every residue of its output columns and so reads the
+// input panel D times over per column span; under an input transpose it reads
+// whole spans of D residues for one.  Either way the operand traffic per tile
+// outgrows the pass's HBM traffic at these widths.  Here the permutations
+// leave the GEMM: an input transpose first de-interleaves the input once
+// (residue g's columns k*D + g become the contiguous block g), both components
+// then run as plain per-block GEMMs: component 2 (W2 on that block-ordered
+// input) into an fp32 slice, then component 1 with the pass's epilogue, which
+// adds the slice, read at the block-order place of each output column
+// (column g*bn + j for output column j*D + g) under an output transpose.  The
+// tokens run in chunks that keep the workspace (slice and de-interleaved
+// input) within 2 GiB.
+template <int BM, int BN, int WGM, int WGN, int D, bool W_T>
+hipError_t launch_permuted_as(const GemmPass &p, bool in_t, bool out_t, hipStream_t s) {
+    const size_t per_tok = (in_t ? (size_t)p.Kin * 2 : 0) + (size_t)p.Nout * sizeof(float);
+    const size_t cap = (size_t)2 << 30;
+    int64_t mc = (int64_t)(cap / per_tok);
+    if (mc >= p.M) mc = p.M;
+    else mc -= mc % 256;
+    if (mc < 1 || (mc < 256 && mc < p.M)) return hipErrorNotSupported;
+    void *ws = nullptr;
+    if (split_workspace(s, per_tok * (size_t)mc, &ws) != hipSuccess) {
+        (void)hipGetLastError();
+        return hipErrorNotSupported;
+    }
+    float *part = static_cast<float *>(ws);
+    uint16_t *xp = reinterpret_cast<uint16_t *>(part + mc * p.Nout);
+    hipError_t e = hipSuccess;
+    for (int64_t m0 = 0; m0 < p.M && e == hipSuccess; m0 += mc) {
+        GemmPass c = p;
+        c.M = p.M - m0 < mc ? p.M - m0 : mc;
+        c.in = static_cast<const uint16_t *>(p.in) + m0 * p.Kin;
+        c.out = static_cast<uint16_t *>(p.out) + m0 * p.Nout;
+        if (p.h_in) c.h_in = static_cast<const uint16_t *>(p.h_in) + m0 * p.Nout;
+        if (p.h_out) c.h_out = static_cast<uint16_t *>(p.h_out) + m0 * p.Nout;
+        GemmPass c2 = c;
+        c2.W1 = p.W2;
+        if (in_t) {
+            e = launch_deinterleave(static_cast<const uint16_t *>(c.in), xp, c.M, p.bk, D, s);
+            c2.in = xp;
+        }
+        if (e == hipSuccess) e = launch_component<BM, BN, WGM, WGN, D, false, false, W_T, 1>(c2, part, 0, false, s);
+        if (e == hipSuccess) e = launch_component<BM, BN, WGM, WGN, D, false, false, W_T, 3>(c, part, 0, out_t, s);
+    }
+    return e;
+}
+
+template <int D, bool IN_T, bool OUT_T, bool W_T>
+hipError_t launch_permuted(const GemmPass &p, hipStream_t s) {
+    if constexpr (D < 8 || 64 % D != 0 || (!IN_T && !OUT_T)) {
+        return hipErrorNotSupported;
+    } else {
+        if (p.bk % kStageK != 0 || p.Nout % 8 != 0) return hipErrorNotSupported;
+        if (p.bn % 256 == 0) return launch_permuted_as<256, 256, 2, 4, D, W_T>(p, IN_T, OUT_T, s);
+        if (p.bn % 128 == 0) return launch_permuted_as<128, 128, 2, 2, D, W_T>(p, IN_T, OUT_T, s);
+        if (p.bn % 64 == 0) return launch_permuted_as<128, 64, 2, 2, D, W_T>(p, IN_T, OUT_T, s);
+        return hipErrorNotSupported;
+    }
+}
+
 template <int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     if (p.bk % kStageK != 0) return hipErrorNotSupported;
     auto enough = [&](int bm, int bn_tile) { return ((p.M + bm - 1) / bm) * (p.Nout / bn_tile) >= 256; };
+    if constexpr (D >= 8)
+        if (permuted_pays(D, OUT_T, W_T, p.M, p.bk)) {
+            const hipError_t e = launch_permuted<D, IN_T, OUT_T, W_T>(p, s);
+            if (e != hipErrorNotSupported) return e;
+        }
     if constexpr (D <= 4) {
         // the fused-stage kernel (natural-layout weights, transpose reads) wins
         // for the input gradient without an output transpose

@@ -254,6 +254,9 @@ __global__ void __launch_bounds__(64 * kSkWaves) skinny_part_kernel(SkArgs a) {
 }
 
 // out[n][f] = epilogue(sum of the slices, in slice order); 8 columns per thread.
+// PERM: the last slice holds its sums in block order, output column j*D + g at
+// column g*bn + j, and is read there.
+template <bool PERM>
 __global__ void __launch_bounds__(256) skinny_reduce_kernel(GemmPass p, const float *part, int slices) {
     const int64_t per_row = p.Nout / 8;
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -268,6 +271,16 @@ __global__ void __launch_bounds__(256) skinny_reduce_kernel(GemmPass p, const fl
         for (int v = 0; v < 4; ++v) { x[v] = lo[v]; x[4 + v] = hi[v]; }
     }
     for (int s = 1; s < slices; ++s) {
+        if (PERM && s == slices - 1) {
+            const float *row = part + s * stride + n * p.Nout;
+            const int D = (int)p.D, bn = (int)p.bn;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                const int c = (int)f + v;
+                x[v] += row[(c % D) * bn + c / D];
+            }
+            continue;
+        }
         const float *src = part + s * stride + e0;
         const f32x4_t lo = *reinterpret_cast<const f32x4_t *>(src);
         const f32x4_t hi = *reinterpret_cast<const f32x4_t *>(src + 4);
@@ -461,10 +474,51 @@ hipError_t split_workspace(hipStream_t s, size_t bytes, void **out) {
     return hipSuccess;
 }
 
-hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s) {
+hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s, bool perm_last) {
     if (p.Nout % 8 != 0) return hipErrorNotSupported;
     const int64_t threads = p.M * (p.Nout / 8);
-    skinny_reduce_kernel<<<(unsigned)((threads + 255) / 256), 256, 0, s>>>(p, part, slices);
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    if (perm_last)
+        skinny_reduce_kernel<true><<<blocks, 256, 0, s>>>(p, part, slices);
+    else
+        skinny_reduce_kernel<false><<<blocks, 256, 0, s>>>(p, part, slices);
+    return hipGetLastError();
+}
+
+// out[n][g*bk + k] = in[n][k*D + g] for a token row of D*bk elements: the
+// input columns of residue g made the contiguous block g.  A group of 4*D
+// threads moves 32 reduction indices of one row (D divides 64): 16-byte loads
+// of the row span into LDS, then per thread 8 indices of one residue, stored
+// as 16 bytes.
+__global__ void __launch_bounds__(256) deinterleave_kernel(const uint16_t *in, uint16_t *out, int64_t M, int bk,
+                                                           int D) {
+    __shared__ uint4 buf[256];
+    const int tid = threadIdx.x, per = 4 * D;
+    const int c = tid / per, pc = tid % per;
+    const int spans = bk / 32;
+    const int64_t gc = (int64_t)blockIdx.x * (256 / per) + c;
+    const bool ok = gc < M * spans;
+    const int64_t n = ok ? gc / spans : 0, kc = ok ? gc % spans : 0;
+    const int64_t Kin = (int64_t)bk * D;
+    if (ok) buf[tid] = *reinterpret_cast<const uint4 *>(in + n * Kin + kc * 32 * D + pc * 8);
+    __syncthreads();
+    if (!ok) return;
+    const int g = pc / 4, k0 = (pc % 4) * 8;
+    const uint16_t *span = reinterpret_cast<const uint16_t *>(buf + c * per);
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)span[(k0 + 2 * e) * D + g] | ((uint32_t)span[(k0 + 2 * e + 1) * D + g] << 16);
+    *reinterpret_cast<uint4 *>(out + n * Kin + (int64_t)g * bk + kc * 32 + k0) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+hipError_t launch_deinterleave(const uint16_t *in, uint16_t *out, int64_t M, int64_t bk, int D, hipStream_t s) {
+    if (D < 1 || 64 % D != 0 || bk % 32 != 0 || M < 0) return hipErrorNotSupported;
+    if (M == 0) return hipSuccess;
+    const int64_t groups = M * (bk / 32), per_block = 256 / (4 * D);
+    const int64_t blocks = (groups + per_block - 1) / per_block;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    deinterleave_kernel<<<(unsigned)blocks, 256, 0, s>>>(in, out, M, (int)bk, D);
     return hipGetLastError();
 }
 
