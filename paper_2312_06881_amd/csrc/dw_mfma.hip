@@ -87,12 +87,14 @@ bool choose(const DwPass &p, DwPlan &pl) {
 // block-ordered copies in the stream's workspace (each at most 2 GiB), and
 // both components then run on the plain tiles, whose operand reads are whole
 // rows of one group instead of spans of all D.  Measured on gfx950 against
-// the fused tiles, this pays from 2048 tokens at n_dyad 16 (1.1-1.6x at
+// the fused tiles, this pays at n_dyad 16 from 2048 tokens (1.1-1.6x at
 // d = 1024, 3-4x on the wide layer 8192 -> 32768 at 32768 tokens) and from
-// 8192 at n_dyad 8 (at 2048 tokens it lost by up to 15%).
+// 256 with blocks of at least 512 (1.8-3.5x on the wide layer at 256 and
+// 1024 tokens), and at n_dyad 8 from 8192 (at 2048 tokens it lost by up to 15%).
 bool dw_permuted(const DwPass &p) {
     if ((p.D != 8 && p.D != 16) || (!p.in_t && !p.out_t)) return false;
-    if (p.M < (p.D == 16 ? 2048 : 8192)) return false;
+    const bool wide = p.D == 16 && p.M >= 256 && p.bi >= 512 && p.bo >= 512;
+    if (!wide && p.M < (p.D == 16 ? 2048 : 8192)) return false;
     if ((p.out_t && p.bo % 32 != 0) || (p.in_t && p.bi % 32 != 0)) return false;
     const int64_t cap = (int64_t)1 << 31;
     return !(p.out_t && p.M * p.n_out * 2 > cap) && !(p.in_t && p.M * p.n_in * 2 > cap);

@@ -99,6 +99,21 @@ hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices,
 // (bk a multiple of 32, D a divisor of 64, 16-byte aligned rows).
 hipError_t launch_deinterleave(const uint16_t *in, uint16_t *out, int64_t M, int64_t bk, int D, hipStream_t s);
 
+// Whether a bf16 pass at n_dyad 8 / 16 with a transpose (exact widths) takes the
+// large-batch form that de-interleaves its input and runs the components as
+// plain per-block GEMMs.  Measured on gfx950 against the fused tiles at 256 to
+// 16384 tokens: at n_dyad 16 it wins from 2048 tokens with reduction blocks of
+// 128 under an output transpose and 256 without, for the input gradient under
+// an output transpose from blocks of 64 once the batch reaches 8192, and from
+// 256 tokens with blocks of 512 (1.6-6.6x on the wide layer 8192 -> 32768 at
+// 1024 tokens); at n_dyad 8 from 2048 tokens with blocks of 512.
+inline bool permuted_pays(int D, bool out_t, bool w_t, int64_t M, int64_t bk) {
+    if (D >= 16 && M >= 256 && bk >= 512) return true;
+    if (M < 2048) return false;
+    if (D >= 16) return bk >= (out_t ? 128 : 256) || (w_t && out_t && M >= 8192 && bk >= 64);
+    return bk >= 512;
+}
+
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
 // when the pass's shape has no matching tile configuration (zero-padded
 // widths included).

@@ -6,16 +6,6 @@
 
 namespace dyad {
 
-// Whether a pass at n_dyad 8 / 16 with a transpose takes launch_permuted
-// (measured on gfx950 against the fused tiles at 2048 and 16384 tokens: at
-// n_dyad 16 it wins from reduction blocks of 128 with an output transpose and
-// from 256 without, and for the input gradient under an output transpose
-// from blocks of 64 once the batch is large; at n_dyad 8 from blocks of 512).
-inline bool permuted_pays(int D, bool out_t, bool w_t, int64_t M, int64_t bk) {
-    if (M < 2048) return false;
-    if (D >= 16) return bk >= (out_t ? 128 : 256) || (w_t && out_t && M >= 8192 && bk >= 64);
-    return bk >= 512;
-}
 
 // Workgroups per CU: two 4-wave workgroups when both the tile's LDS and its
 // registers fit twice (two caps a wave at 256 VGPRs, so accumulators above 128
@@ -287,6 +277,8 @@ hipError_t launch_permuted(const GemmPass &p, hipStream_t s) {
         return hipErrorNotSupported;
     } else {
         if (p.bk % kStageK != 0 || p.Nout % 8 != 0) return hipErrorNotSupported;
+        // up to 1024 tokens, 128-token tiles: twice the workgroups, the weights read twice
+        if (p.bn % 256 == 0 && p.M <= 1024) return launch_permuted_as<128, 256, 2, 4, D, W_T>(p, IN_T, OUT_T, s);
         if (p.bn % 256 == 0) return launch_permuted_as<256, 256, 2, 4, D, W_T>(p, IN_T, OUT_T, s);
         if (p.bn % 128 == 0) return launch_permuted_as<128, 128, 2, 2, D, W_T>(p, IN_T, OUT_T, s);
         if (p.bn % 64 == 0) return launch_permuted_as<128, 64, 2, 2, D, W_T>(p, IN_T, OUT_T, s);
@@ -299,7 +291,7 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     if (p.bk % kStageK != 0) return hipErrorNotSupported;
     auto enough = [&](int bm, int bn_tile) { return ((p.M + bm - 1) / bm) * (p.Nout / bn_tile) >= 256; };
     if constexpr (D >= 8)
-        if (permuted_pays(D, OUT_T, W_T, p.M, p.bk)) {
+        if (permuted_pays((int)D, OUT_T, W_T, p.M, p.bk)) {
             const hipError_t e = launch_permuted<D, IN_T, OUT_T, W_T>(p, s);
             if (e != hipErrorNotSupported) return e;
         }

@@ -136,3 +136,48 @@ def test_backward_dw_full(shape, variant):
     assert_close(dw1, r1, "bf16", "dW1")
     assert_close(dw2, r2, "bf16", "dW2")
     assert_close(db, rb, "bf16", "db")
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_wide_blocks_few_hundred_tokens(variant):
+    """Blocks of 512 at n_dyad 16 with 300 tokens (the large-batch path from
+    256 tokens on such blocks: 128-token tiles, a ragged last one): forward
+    with GELU, input gradient with GELU', weight gradients, element by
+    element."""
+    n_in, n_out, D, M = 8192, 8192, 16, 300
+    banner("permuted_few_hundred", variant)
+    L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=9)
+    y, h = dy.forward(gpu(L.X), gpu(L.W1), gpu(L.W2), gpu(L.bias), variant=variant, act="gelu", stash_h=True)
+    dx = dy.backward_dx(gpu(L.dZ), gpu(L.W1), gpu(L.W2), variant=variant, act_in="gelu", h_in=gpu(L.H_in))
+    dw1, dw2, db = dy.backward_dw(gpu(L.dZ), gpu(L.X), D, variant=variant)
+    torch.cuda.synchronize()
+    W1, W2 = L.f64("W1"), L.f64("W2")
+    ry, rh = oracle.forward(variant, n_in, n_out, D, L.f64("X"), W1, W2, L.f64("bias"), act=oracle.ACT_GELU,
+                            want_h=True)
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, L.f64("dZ"), W1, W2, act_in=oracle.ACT_GELU,
+                             H_in=L.f64("H_in"))
+    r1, r2, rb = oracle.backward_dw(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"))
+    assert_close(y, ry, "bf16", "Y")
+    assert_close(h, rh, "bf16", "H")
+    assert_close(dx, rdx, "bf16", "dX")
+    assert_close(dw1, r1, "bf16", "dW1")
+    assert_close(dw2, r2, "bf16", "dW2")
+    assert_close(db, rb, "bf16", "db")
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_wide_blocks_1030_tokens_sampled(variant):
+    """The same layer with 1030 tokens (256-token tiles from 1025 tokens),
+    forward and input gradient on sampled rows."""
+    n_in, n_out, D, M = 8192, 8192, 16, 1030
+    banner("permuted_1030", variant)
+    L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=10)
+    y = dy.forward(gpu(L.X), gpu(L.W1), gpu(L.W2), gpu(L.bias), variant=variant)
+    dx = dy.backward_dx(gpu(L.dZ), gpu(L.W1), gpu(L.W2), variant=variant)
+    torch.cuda.synchronize()
+    rows = np.array(sorted({0, 1, 255, 256, 511, 767, 768, 1023, 1024, M - 1}))
+    W1, W2 = L.f64("W1"), L.f64("W2")
+    ry = oracle.forward(variant, n_in, n_out, D, L.X[rows].to(torch.float64).numpy(), W1, W2, L.f64("bias"))
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, L.dZ[rows].to(torch.float64).numpy(), W1, W2)
+    assert_close(y[rows], ry, "bf16", "Y rows")
+    assert_close(dx[rows], rdx, "bf16", "dX rows")
