@@ -279,8 +279,12 @@ hipError_t launch_permuted(const GemmPass &p, hipStream_t s) {
         if (p.bk % kStageK != 0 || p.Nout % 8 != 0) return hipErrorNotSupported;
         // up to 1024 tokens, 128-token tiles: twice the workgroups, the weights
         // read twice; 128 x 128 where 128 x 256 would not give every CU a tile
-        // (1.2x at 256 and 512 tokens, wide layer fc2 forward / fc1 input gradient)
+        // (1.2x at 256 and 512 tokens, wide layer fc2 forward / fc1 input
+        // gradient), and up to 512 tokens 64 x 128 where 128 x 128 would not
+        // (another 1.1-1.2x at 256 tokens)
         const int64_t tm = (p.M + 127) / 128;
+        if (p.bn % 128 == 0 && p.M <= 512 && tm * (p.Nout / 128) < 256)
+            return launch_permuted_as<64, 128, 2, 2, D, W_T>(p, IN_T, OUT_T, s);
         if (p.bn % 128 == 0 && p.M <= 1024 && tm * (p.Nout / 256) < 256)
             return launch_permuted_as<128, 128, 2, 2, D, W_T>(p, IN_T, OUT_T, s);
         if (p.bn % 256 == 0 && p.M <= 1024) return launch_permuted_as<128, 256, 2, 4, D, W_T>(p, IN_T, OUT_T, s);
