@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--block", default="",
                     help="instead of the layer step: time an OPT-125m-shaped decoder block fwd+bwd "
                          "(dense, Dyad FF only, Dyad everywhere) with this variant (IT/OT/DT)")
+    ap.add_argument("--sets", type=int, default=0,
+                    help="buffer sets to rotate (default: enough that a set recurs after ~512 MiB of traffic)")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("CALL", "FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs of --only CALL (FETCH_SIZE, WRITE_SIZE) into "
                          "profiles/traffic_<workload>.json")
@@ -233,8 +235,17 @@ def main():
     else:
         (_, i1, o1), = wl.layers
         i2, o2 = o1, i1
-    fc1 = Layer(torch, i1, o1, D, M, 0, dev)
-    fc2 = Layer(torch, i2, o2, D, M, 1, dev)
+    # Buffer sets, rotated call by call: consecutive calls never touch the same
+    # buffers, and a set comes round again only after about 512 MiB of other
+    # calls' traffic (twice the 256 MB last-level cache), so small-batch calls
+    # read their weights from HBM, not from the cache.
+    mean_call = sum(algorithmic_bytes(k, n_in, n_out, D, M) for (_, n_in, n_out) in
+                    ((None, i1, o1), (None, i2, o2)) for k in ("fwd", "dx", "dw")) / 6
+    n_sets = max(1, min(16, -(-(512 << 20) // int(mean_call))))
+    if args.sets:
+        n_sets = args.sets
+    layers = [(Layer(torch, i1, o1, D, M, 0, dev), Layer(torch, i2, o2, D, M, 1, dev)) for _ in range(n_sets)]
+    fc1, fc2 = layers[0]
     ws_bytes = max(dy.dyad_dw_workspace_bytes(vid[v], L.n_in, L.n_out, D, M, dy.BF16)
                    for v in variants for L in (fc1, fc2))
     ws = torch.empty((max(ws_bytes, 16),), dtype=torch.uint8, device=dev)
@@ -243,27 +254,33 @@ def main():
         if rc != 0:
             raise RuntimeError(dy.dyad_strerror(rc))
 
-    calls = build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp)
+    sets = [build_calls(dy, lib, wl, a, b, variants, ws, ws_bytes, sp) for a, b in layers]
+    calls = sets[0]
+    n_calls = len(calls)
     if args.only:
         # counter collection: one call, repeated, plus a plain copy of known size
-        sel = [c for c in calls if c[0] == args.only]
-        if not sel:
+        idx = [i for i, c in enumerate(calls) if c[0] == args.only]
+        if not idx:
             raise SystemExit(f"--only {args.only}: no such call; one of {[c[0] for c in calls]}")
-        src = torch.empty((256 << 20,), dtype=torch.uint8, device=dev)
+        src = torch.empty((COPY_BYTES,), dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
-        for _ in range(args.steps):
-            check(sel[0][3]())
+        for r in range(args.steps):
+            check(sets[r % n_sets][idx[0]][3]())
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"only": args.only, "launches": args.steps, "copy_bytes": src.numel(),
-                          "algorithmic_bytes": sel[0][2], "flops": sel[0][1]}))
+                          "buffer_sets": n_sets, "algorithmic_bytes": calls[idx[0]][2],
+                          "flops": calls[idx[0]][1]}))
         return
 
     flops_step = sum(c[1] for c in calls)
+    rot = [0]
 
     def step():
-        for c in calls:
-            check(c[3]())
+        # call c of the step takes the next buffer set in turn
+        for c in range(n_calls):
+            check(sets[rot[0] % n_sets][c][3]())
+            rot[0] += 1
 
     for _ in range(args.warmup):
         step()
@@ -283,26 +300,34 @@ def main():
     ms_step = t0.elapsed_time(t1) / args.steps
     tflops = flops_step / (ms_step * 1e-3) / 1e12
 
-    # per-call durations: K more steps with an event pair around every call
+    # per-call durations: at least 50 more steps with an event pair around every call
+    reps = max(50, args.steps)
     evs = []
-    for _ in range(args.steps):
-        for c in calls:
+    for _ in range(reps):
+        for c in range(n_calls):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            call = sets[rot[0] % n_sets][c]
+            rot[0] += 1
             a.record(stream)
-            check(c[3]())
+            check(call[3]())
             b.record(stream)
-            evs.append((c, a, b))
+            evs.append((call, a, b))
     torch.cuda.synchronize()
     per = {}
     for c, a, b in evs:
-        d = per.setdefault(c[0], {"ms": 0.0, "n": 0, "flops": c[1], "bytes": c[2]})
-        d["ms"] += a.elapsed_time(b)
-        d["n"] += 1
+        d = per.setdefault(c[0], {"t": [], "flops": c[1], "bytes": c[2]})
+        d["t"].append(a.elapsed_time(b))
     table = {}
     for name, d in per.items():
+        t = sorted(d["t"])
+        d["ms"] = sum(t)
+        d["n"] = len(t)
         us = d["ms"] / d["n"] * 1e3
-        table[name] = {"us": round(us, 2), "tflops": round(d["flops"] / (us * 1e-6) / 1e12, 1),
-                       "gbs": round(d["bytes"] / (us * 1e-6) / 1e9, 1),
+        q = lambda f: t[min(len(t) - 1, int(f * (len(t) - 1) + 0.5))] * 1e3  # noqa: E731
+        table[name] = {"us": round(us, 2), "us_median": round(q(0.5), 2), "us_p10": round(q(0.1), 2),
+                       "us_p90": round(q(0.9), 2), "reps": len(t),
+                       "tflops": round(d["flops"] / (q(0.5) * 1e-6) / 1e12, 1),
+                       "gbs": round(d["bytes"] / (q(0.5) * 1e-6) / 1e9, 1),
                        "bound": "hbm" if d["flops"] / d["bytes"] < RIDGE else "mfma"}
     dom = max(per, key=lambda n: per[n]["ms"])
     dd = per[dom]
@@ -341,14 +366,16 @@ def main():
         "config": {"workload": wl.name, "description": wl.note, "n_dyad": D, "tokens": M,
                    "layers": [list(l) for l in wl.layers], "variants": variants,
                    "step": "per variant: fc1 fwd(GELU, stash) + fc2 fwd + fc2 dX(GELU') + fc2 dW+db "
-                           "+ fc1 dX + fc1 dW+db"},
+                           "+ fc1 dX + fc1 dW+db",
+                   "buffer_sets": n_sets},
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "per_variant": per_variant,
         "speedup_vs_dense": dense["speedup"] if dense else None,
         "dense": dense,
         "roofline": {"bound": table[dom]["bound"], "call": dom, "achieved": round(achieved, 1),
                      "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
-                     "avg_launch_us": round(avg_s * 1e6, 2), "flops_per_launch": dd["flops"],
+                     "avg_launch_us": round(avg_s * 1e6, 2), "median_launch_us": table[dom]["us_median"],
+                     "flops_per_launch": dd["flops"],
                      "bytes_per_launch": dd["bytes"],
                      "traffic": read_traffic(dom, wl.name)},
         "per_call": table,
@@ -391,17 +418,20 @@ def dense_baseline(torch, fc1, fc2, M, dev, stream, args):
 
 
 def cpu_baseline(wl, tokens):
-    """The oracle, as it stands, on the first `tokens` tokens of the same workload (Dyad-IT)."""
+    """The oracle, as it stands, on the first `tokens` tokens of the same workload (Dyad-IT).
+    The inputs are drawn before the clock starts; only the oracle's passes are timed."""
     import oracle
     from workloads import layer_inputs
     D = wl.n_dyad
     Ms = min(tokens, wl.M)
-    flops = 0.0
-    t0 = time.perf_counter()
+    inputs = []
     for li, (_, n_in, n_out) in enumerate(wl.layers):
         L = layer_inputs(n_in, n_out, D, Ms, "bf16", seed_offset=li)
-        X, W1, W2, dZ = L.f64("X"), L.f64("W1"), L.f64("W2"), L.f64("dZ")
-        oracle.forward("IT", n_in, n_out, D, X, W1, W2, L.f64("bias"))
+        inputs.append((n_in, n_out, L.f64("X"), L.f64("W1"), L.f64("W2"), L.f64("dZ"), L.f64("bias")))
+    flops = 0.0
+    t0 = time.perf_counter()
+    for n_in, n_out, X, W1, W2, dZ, b in inputs:
+        oracle.forward("IT", n_in, n_out, D, X, W1, W2, b)
         oracle.backward_dx("IT", n_in, n_out, D, dZ, W1, W2)
         oracle.backward_dw("IT", n_in, n_out, D, dZ, X)
         flops += 3 * 4.0 * Ms * n_in * n_out / D
@@ -409,7 +439,7 @@ def cpu_baseline(wl, tokens):
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle", "seconds": round(dt, 2),
             "sample": f"{wl.name}, Dyad-IT only, every layer fwd + dX + dW + db on {Ms} of {wl.M} "
-                      f"tokens (fp64 plain loops, OpenMP); input generation included"}
+                      f"tokens (fp64 plain loops, OpenMP); inputs drawn before the timer"}
 
 
 COPY_BYTES = 256 << 20   # the plain copy --only runs beside the call, for counter calibration

@@ -28,22 +28,23 @@
  * bf16 results are rounded to nearest even.
  *
  * Ownership and ordering: the caller allocates and owns every buffer, the
- * dW workspace included.  The library also keeps intermediates of its own in
- * a library-owned device buffer, one per (device, stream), taken in stream
- * order from a per-device memory pool of the current device the first time
- * that stream needs it, regrown in stream order when a later call needs more,
- * and kept until the process ends.  It holds: the fp32 partial sums of
- * dyad_forward and dyad_backward_dx when they split their reduction over
- * workgroups (small batches, few output tiles; a few slices of M x n_out
- * fp32, at most 2 GiB); for those two calls at n_dyad 8 / 16 with large
- * batches, a de-interleaved copy of the input and one fp32 slice of the
- * output (at most 2 GiB, the tokens taken in chunks beyond that); and for
- * dyad_backward_dw at n_dyad 8 / 16 with large batches, de-interleaved copies
- * of dZ and / or X (each at most 2 GiB, so at most 4 GiB).  Calls on one
- * stream share it in stream order; calls on different streams never share
- * it.  When it cannot be had, dyad_forward and dyad_backward_dx run without
- * the split or the copy; dyad_backward_dw runs without the copies if the
- * workspace passed in also fits that form, else it fails with DYAD_ERR_LAUNCH.
+ * dW workspace included; dyad_backward_dw allocates nothing (its fp32 partial
+ * sums and, at n_dyad 8 / 16 with large batches, the de-interleaved copies of
+ * dZ and / or X all live in the workspace the caller passes).
+ * dyad_forward and dyad_backward_dx are the one bounded departure from
+ * "caller owns everything": they may keep intermediates in a library-owned
+ * device buffer, one per (device, stream), taken in stream order from a
+ * per-device memory pool the first time that stream needs it, regrown in
+ * stream order when a later call needs more, and kept until the process
+ * ends.  It holds the fp32 partial sums of a split reduction (small batches,
+ * few output tiles; a few slices of M x n_out fp32, at most 2 GiB) and, at
+ * n_dyad 8 / 16 with large batches, a de-interleaved copy of the input and
+ * one fp32 slice of the output (at most 2 GiB; the tokens are taken in chunks
+ * beyond that).  Calls on one stream share it in stream order; calls on
+ * different streams never share it.  While the stream is being captured into
+ * a graph the buffer is never allocated or regrown; when it cannot be had
+ * (capture, or the pool fails), the call runs a plan that needs none, with
+ * the same results.
  * Every call only enqueues work on `stream`
  * (NULL = the null stream) and returns without synchronising; results are
  * valid once that work completes.  Outputs are overwritten, never accumulated
@@ -75,7 +76,7 @@ typedef enum {
     DYAD_ERR_ALIGN = -3,       /* a non-NULL pointer is not 16-byte aligned */
     DYAD_ERR_DTYPE = -4,       /* unknown dtype */
     DYAD_ERR_WORKSPACE = -5,   /* dW workspace NULL or smaller than dyad_dw_workspace_bytes() */
-    DYAD_ERR_LAUNCH = -6,      /* the HIP runtime rejected a kernel launch or a library-owned buffer */
+    DYAD_ERR_LAUNCH = -6,      /* the HIP runtime rejected a kernel launch */
 } dyad_status;
 
 /*

@@ -10,7 +10,7 @@ paper); this module only marshals numpy float64 arrays into it.
 
 Parity is pinned by the ``-m "not gpu"`` tests against things other than the
 oracle itself: a dense weight built from the permutation matrix of Eq. 5,
-a numpy restatement of the paper's reshape/transpose/bmm formulation, the
+a gather / batched-product / scatter form built from the index definitions, the
 n_dyad=1 collapse to a dense layer, the parameter counts the paper prints,
 finite differences for the backward pass, and ``math.erf`` for GELU.
 """

@@ -84,7 +84,7 @@ bool choose(const DwPass &p, DwPlan &pl) {
 
 // Large batches at n_dyad 8 and 16 with a transpose: component 2's strided
 // operands (dZ columns j*D + g, X columns k*D + g) are de-interleaved once into
-// block-ordered copies in the stream's workspace (each at most 2 GiB), and
+// block-ordered copies in the caller's workspace (each at most 2 GiB), and
 // both components then run on the plain tiles, whose operand reads are whole
 // rows of one group instead of spans of all D.  Measured on gfx950 against
 // the fused tiles, this pays at n_dyad 16 from 2048 tokens (1.1-1.6x at
@@ -128,10 +128,23 @@ static size_t plan_workspace(const DwPass &p, const DwPlan &pl) {
     return (size_t)pl.splits * (size_t)(2 * p.D * p.bo * p.bi + p.n_out) * sizeof(float);
 }
 
+static size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Bytes of the block-ordered copies of the permuted form: dZ under an output
+// transpose, X under an input transpose.
+static size_t copy_bytes_z(const DwPass &p) { return p.out_t ? (size_t)p.M * (size_t)p.n_out * 2 : 0; }
+static size_t copy_bytes_x(const DwPass &p) { return p.in_t ? (size_t)p.M * (size_t)p.n_in * 2 : 0; }
+
+// Workspace of the plan a pass runs with: the partial sums, then (permuted
+// form) the copies, each starting on a 256-byte boundary.  The library
+// allocates nothing for the weight gradient; all of it comes from the caller.
 size_t mfma_dw_workspace(const DwPass &p) {
     DwPlan pl;
     bool permuted;
-    return plan(p, pl, &permuted) ? plan_workspace(p, pl) : 0;
+    if (!plan(p, pl, &permuted)) return 0;
+    size_t b = plan_workspace(p, pl);
+    if (permuted) b = round256(b) + round256(copy_bytes_z(p)) + copy_bytes_x(p);
+    return b;
 }
 
 hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s) {
@@ -139,28 +152,24 @@ hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s) {
     bool permuted;
     if (!plan(p, pl, &permuted)) return hipErrorNotSupported;
     if (permuted) {
-        const size_t zb = p.out_t ? (size_t)p.M * (size_t)p.n_out * 2 : 0;
-        const size_t xb = p.in_t ? (size_t)p.M * (size_t)p.n_in * 2 : 0;
-        void *ws = nullptr;
-        hipError_t e = split_workspace(s, zb + xb, &ws);
-        if (e == hipSuccess) {
-            DwPass q = p;
-            q.in_t = q.out_t = false;
-            uint16_t *z2 = static_cast<uint16_t *>(ws), *x2 = z2 + zb / 2;
-            if (p.out_t) {
-                e = launch_deinterleave(static_cast<const uint16_t *>(p.dZ), z2, p.M, p.bo, (int)p.D, s);
-                q.dZ2 = z2;
-            }
-            if (e == hipSuccess && p.in_t) {
-                e = launch_deinterleave(static_cast<const uint16_t *>(p.X), x2, p.M, p.bi, (int)p.D, s);
-                q.X2 = x2;
-            }
-            return e == hipSuccess ? launch_dw_plain(q, pl, s) : e;
+        // the caller's workspace holds mfma_dw_workspace(p) bytes (checked by
+        // the C-ABI): partial sums first, then the copies
+        DwPass q = p;
+        q.in_t = q.out_t = false;
+        const size_t zoff = round256(plan_workspace(p, pl));
+        uint16_t *z2 = reinterpret_cast<uint16_t *>(static_cast<unsigned char *>(p.ws) + zoff);
+        uint16_t *x2 = reinterpret_cast<uint16_t *>(reinterpret_cast<unsigned char *>(z2) +
+                                                    round256(copy_bytes_z(p)));
+        hipError_t e = hipSuccess;
+        if (p.out_t) {
+            e = launch_deinterleave(static_cast<const uint16_t *>(p.dZ), z2, p.M, p.bo, (int)p.D, s);
+            q.dZ2 = z2;
         }
-        // no room for the copies: the fused form, if the caller's workspace
-        // (sized for the plan above) also holds that plan's partial sums
-        if (!choose(p, pl) || plan_workspace(p, pl) > p.ws_bytes) return e;
-        (void)hipGetLastError();
+        if (e == hipSuccess && p.in_t) {
+            e = launch_deinterleave(static_cast<const uint16_t *>(p.X), x2, p.M, p.bi, (int)p.D, s);
+            q.X2 = x2;
+        }
+        return e == hipSuccess ? launch_dw_plain(q, pl, s) : e;
     }
     if (p.in_t && !p.out_t) return launch_dw_it(p, pl, s);
     if (!p.in_t && p.out_t) return launch_dw_ot(p, pl, s);

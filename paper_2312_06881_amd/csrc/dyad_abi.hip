@@ -3,6 +3,8 @@
 // the first HIP call.
 #include "dyad.h"
 
+#include <string.h>
+
 #include "dyad_internal.h"
 
 namespace {
@@ -15,6 +17,18 @@ constexpr int64_t kMaxElems = (int64_t)1 << 40; // any single tensor, in element
 
 // Per-block size; a width that D does not divide is zero-padded up to D blocks.
 int64_t block(int64_t n, int64_t D) { return (n + D - 1) / D; }
+
+// The int a caller passed for an enum parameter.  A C caller may pass any
+// int there; reading the parameter through its enum type would be undefined
+// in C++ for values outside the enumerators' range, so its bytes are read as
+// an int and every check works on that.
+template <class E>
+int enum_value(const E &e) {
+    static_assert(sizeof(E) == sizeof(int), "C enums are int-sized");
+    int v;
+    memcpy(&v, &e, sizeof v);
+    return v;
+}
 
 bool aligned16(const void *p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
 
@@ -54,9 +68,10 @@ size_t dw_workspace(const DwPass &p) {
 
 extern "C" {
 
-int dyad_forward(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
-                 dyad_dtype dtype, const void *X, const void *W1, const void *W2, const void *bias,
-                 dyad_act act, void *Y, void *H, hipStream_t stream) {
+int dyad_forward(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                 dyad_dtype dtype_arg, const void *X, const void *W1, const void *W2, const void *bias,
+                 dyad_act act_arg, void *Y, void *H, hipStream_t stream) {
+    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg), act = enum_value(act_arg);
     int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
     if (rc) return rc;
     if (act != DYAD_ACT_NONE && act != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
@@ -75,9 +90,10 @@ int dyad_forward(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dy
     return run_gemm(p, stream);
 }
 
-int dyad_backward_dx(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
-                     dyad_dtype dtype, const void *dZ, const void *W1, const void *W2, dyad_act act_in,
+int dyad_backward_dx(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype_arg, const void *dZ, const void *W1, const void *W2, dyad_act act_in_arg,
                      const void *H_in, void *dX, hipStream_t stream) {
+    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg), act_in = enum_value(act_in_arg);
     int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
     if (rc) return rc;
     if (act_in != DYAD_ACT_NONE && act_in != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
@@ -103,15 +119,17 @@ static DwPass make_dw(int variant, int64_t n_in, int64_t n_out, int64_t D, int64
     return p;
 }
 
-size_t dyad_dw_workspace_bytes(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad,
-                               int64_t M, dyad_dtype dtype) {
+size_t dyad_dw_workspace_bytes(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad,
+                               int64_t M, dyad_dtype dtype_arg) {
+    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg);
     if (check_sizes(variant, n_in, n_out, n_dyad, M, dtype)) return 0;
     return dw_workspace(make_dw(variant, n_in, n_out, n_dyad, M, dtype));
 }
 
-int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
-                     dyad_dtype dtype, const void *dZ, const void *X, void *dW1, void *dW2, void *dbias,
+int dyad_backward_dw(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype_arg, const void *dZ, const void *X, void *dW1, void *dW2, void *dbias,
                      void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg);
     int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
     if (rc) return rc;
     if (!dW1 || !dW2 || (M > 0 && (!dZ || !X))) return DYAD_ERR_INVALID_ARG;

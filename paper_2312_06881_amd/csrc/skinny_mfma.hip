@@ -456,6 +456,13 @@ hipError_t split_workspace(hipStream_t s, size_t bytes, void **out) {
         *out = w->ptr;
         return hipSuccess;
     }
+    // No allocation (or regrowth) while the stream is being captured into a
+    // graph: the buffer would belong to the graph, not to later eager calls.
+    // The caller then takes a plan that needs no buffer.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    e = hipStreamIsCapturing(s, &cap);
+    if (e != hipSuccess) return e;
+    if (cap != hipStreamCaptureStatusNone) return hipErrorNotSupported;
     hipMemPool_t pool;
     e = pool_of(dev, &pool);
     if (e != hipSuccess) return e;

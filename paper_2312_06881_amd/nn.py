@@ -1,10 +1,10 @@
 """Drop-in torch modules over libdyad.
 
 * ``DyadLinear``: one Dyad layer, y = W x + b with W = BlockDiag(W1) +
-  BlockTrans(W2) in the IT / OT / DT form (paper Sec. 3, Eqs. 1-16), a
+  BlockTrans(W2) in the IT / OT / DT form (paper Sec. 2.2-2.4, Eqs. 1-16), a
   replacement for ``torch.nn.Linear``.
 * ``DyadFF``: the feed-forward block fc1 -> GELU -> fc2 with both layers Dyad,
-  each with its own variant if wanted (a heterogeneous mix, Sec. 5).  The
+  each with its own variant if wanted (a heterogeneous mix, Sec. 4).  The
   forward writes GELU(fc1) and stashes fc1's pre-activation in the same
   epilogue; the backward applies GELU' inside fc2's input-gradient epilogue,
   so the activation gradient is never a separate pass.

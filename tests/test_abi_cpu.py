@@ -130,3 +130,36 @@ def test_dw_workspace_single_split():
     a = dict(variant=0, n_in=768, n_out=3072, n_dyad=4, M=16384, dtype=1, dZ=FAKE, X=FAKE,
              dW1=FAKE, dW2=FAKE, dbias=None, workspace=None, workspace_bytes=0, stream=None)
     assert dy.dyad_backward_dw(**a) == -5
+
+
+def _r256(b):
+    return (b + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("n_in,n_out,D,M", [(1024, 4096, 16, 16384), (4096, 1024, 16, 2048),
+                                            (8192, 32768, 16, 32768), (2048, 8192, 8, 16384),
+                                            (8192, 8192, 16, 300)])
+def test_dw_workspace_holds_the_copies(n_in, n_out, D, M):
+    """At n_dyad 8 / 16 with large batches the weight gradient de-interleaves the strided
+    operands into block-ordered copies; they live in the caller's workspace: partial sums
+    (a whole number of [2 D bo bi + n_out] fp32 splits, possibly none), then the dZ copy
+    (output transpose) on a 256-byte boundary, then the X copy (input transpose)."""
+    ws = {v: dy.dyad_dw_workspace_bytes(dy.VARIANTS[v], n_in, n_out, D, M, dy.BF16) for v in ("IT", "OT", "DT")}
+    zb, xb = M * n_out * 2, M * n_in * 2
+    part = ws["IT"] - xb                     # IT: X copy only
+    assert part >= 0 and part % 256 == 0
+    assert ws["OT"] == part + _r256(zb)      # OT: dZ copy only
+    assert ws["DT"] == part + _r256(zb) + xb
+    split_bytes = 4 * (2 * n_in * n_out // D + n_out)
+    assert part == 0 or part >= split_bytes
+    # without a transpose nothing is copied: the partial sums alone (same plan)
+    ws_plain = dy.dyad_dw_workspace_bytes(dy.IT, n_in, n_out, 1, M, dy.BF16)
+    assert ws_plain % (4 * (2 * n_in * n_out + n_out)) == 0
+
+
+def test_dw_workspace_small_batch_has_no_copies():
+    """Below the large-batch threshold the fused kernels read the strided operands in place."""
+    split_bytes = 4 * (2 * 1024 * 4096 // 16 + 4096)
+    for v in ("IT", "OT", "DT"):
+        b = dy.dyad_dw_workspace_bytes(dy.VARIANTS[v], 1024, 4096, 16, 512, dy.BF16)
+        assert b % split_bytes == 0    # whole splits of partial sums, nothing else

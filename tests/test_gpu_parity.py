@@ -314,36 +314,74 @@ def sample_rows(M, n, seed):
     return np.array(sorted(rows))
 
 
-def check_full_layer(n_in, n_out, D, M, variant, act, seed_offset=0):
+def _f64_rows(t, lo, hi):
+    return t[lo:hi].to(torch.float64).numpy()
+
+
+def oracle_dw_sampled(variant, n_in, n_out, D, dZ, X, comp, i, j, k, chunk=4096):
+    """Sampled dW entries and the full db from the oracle, the token sum taken in chunks of
+    `chunk` tokens (each entry is linear in the tokens, so the chunk results add up to the
+    whole sum) to keep the fp64 copies of very large dZ / X bounded."""
+    M = dZ.shape[0]
+    ent = np.zeros(len(comp), np.float64)
+    db = np.zeros(n_out, np.float64)
+    for lo in range(0, M, chunk):
+        hi = min(M, lo + chunk)
+        z, x = _f64_rows(dZ, lo, hi), _f64_rows(X, lo, hi)
+        ent += oracle.backward_dw_entries(variant, n_in, n_out, D, z, x, comp, i, j, k)
+        db += oracle.bias_grad(z)
+    return ent, db
+
+
+def check_full_layer(n_in, n_out, D, M, variant, fwd_act="none", dx_act="none", seed_offset=0):
+    """One layer at full size, every pass as the bench calls it: forward with `fwd_act`
+    (GELU with the pre-activation stashed when "gelu"), input gradient with `dx_act`
+    (GELU' of H_in when "gelu"), weight and bias gradients.  Checked on 40 sampled tokens
+    (plus the first and last two) and 300 sampled dW entries (corners included), each
+    entry a full sum over all M tokens."""
     L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=seed_offset)
     x, w1, w2, b, dz = (gpu(t) for t in (L.X, L.W1, L.W2, L.bias, L.dZ))
-    h_in = gpu(L.H_in) if act == "gelu" else None
-    y, h = dy.forward(x, w1, w2, b, variant=variant, act=act, stash_h=True)
-    dx = dy.backward_dx(dz, w1, w2, variant=variant, act_in=act, h_in=h_in)
+    h_in = gpu(L.H_in) if dx_act == "gelu" else None
+    if fwd_act == "gelu":
+        y, h = dy.forward(x, w1, w2, b, variant=variant, act="gelu", stash_h=True)
+    else:
+        y, h = dy.forward(x, w1, w2, b, variant=variant), None
+    dx = dy.backward_dx(dz, w1, w2, variant=variant, act_in=dx_act, h_in=h_in)
     dw1, dw2, db = dy.backward_dw(dz, x, D, variant=variant)
     torch.cuda.synchronize()
+    del x, dz, h_in
     rows = sample_rows(M, 40, 7)
     W1, W2 = L.f64("W1"), L.f64("W2")
     Xs = L.X[rows].to(torch.float64).numpy()
-    ry, rh = oracle.forward(variant, n_in, n_out, D, Xs, W1, W2, L.f64("bias"), act=ACT[act],
+    ry, rh = oracle.forward(variant, n_in, n_out, D, Xs, W1, W2, L.f64("bias"), act=ACT[fwd_act],
                             want_h=True)
     assert_close(y[rows], ry, "bf16", "Y rows")
-    if act == "gelu":
+    if fwd_act == "gelu":
         assert_close(h[rows], rh, "bf16", "H rows")
+    del y, h
     dZs = L.dZ[rows].to(torch.float64).numpy()
-    Hs = L.H_in[rows].to(torch.float64).numpy() if act == "gelu" else None
-    rdx = oracle.backward_dx(variant, n_in, n_out, D, dZs, W1, W2, act_in=ACT[act], H_in=Hs)
+    Hs = L.H_in[rows].to(torch.float64).numpy() if dx_act == "gelu" else None
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, dZs, W1, W2, act_in=ACT[dx_act], H_in=Hs)
     assert_close(dx[rows], rdx, "bf16", "dX rows")
+    del dx
     rng = np.random.default_rng(11)
     n = 300
+    bo, bi = n_out // D, n_in // D
     comp = rng.integers(1, 3, n)
-    i, j, k = rng.integers(0, D, n), rng.integers(0, n_out // D, n), rng.integers(0, n_in // D, n)
-    comp[:4], i[:4], j[:4], k[:4] = [1, 2, 1, 2], [0, 0, D - 1, D - 1], [0, 0, n_out // D - 1, n_out // D - 1], [0, 0, n_in // D - 1, n_in // D - 1]
-    ref = oracle.backward_dw_entries(variant, n_in, n_out, D, L.f64("dZ"), L.f64("X"), comp, i, j, k)
-    got = np.where(comp == 1, to64(dw1)[i, j, k], to64(dw2)[i, j, k])
+    i, j, k = rng.integers(0, D, n), rng.integers(0, bo, n), rng.integers(0, bi, n)
+    comp[:4], i[:4], j[:4], k[:4] = [1, 2, 1, 2], [0, 0, D - 1, D - 1], [0, 0, bo - 1, bo - 1], [0, 0, bi - 1, bi - 1]
+    ref, rdb = oracle_dw_sampled(variant, n_in, n_out, D, L.dZ, L.X, comp, i, j, k)
+    ti, tj, tk = (torch.as_tensor(a, device=DEV) for a in (i, j, k))
+    got = np.where(comp == 1, to64(dw1[ti, tj, tk]), to64(dw2[ti, tj, tk]))
     # sampled entries: compare against the scale of the whole sampled set
     assert_close(got, ref, "bf16", "dW entries")
-    assert_close(db, oracle.bias_grad(L.f64("dZ")), "bf16", "db")
+    assert_close(db, rdb, "bf16", "db")
+
+
+# The feed-forward block as the bench runs it: fc1 forward with GELU and the
+# pre-activation stash, fc1 input gradient plain; fc2 forward plain, fc2 input
+# gradient with GELU' of fc1's pre-activation.
+FF_ACTS = {"fc1": ("gelu", "none"), "fc2": ("none", "gelu")}
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
@@ -351,8 +389,8 @@ def check_full_layer(n_in, n_out, D, M, variant, act, seed_offset=0):
 def test_full_size_ff_sampled(wl, variant):
     for li, (name, n_in, n_out) in enumerate(wl.layers):
         banner("full", wl.name, name, variant)
-        check_full_layer(n_in, n_out, wl.n_dyad, wl.M, variant, "gelu" if name == "fc2" else "none",
-                         seed_offset=li)
+        fa, da = FF_ACTS[name]
+        check_full_layer(n_in, n_out, wl.n_dyad, wl.M, variant, fa, da, seed_offset=li)
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
@@ -373,13 +411,18 @@ def test_backward_dw_many_splits(shape, variant):
 
 # ---- width/block sweep and the wide layer, full size, sampled ---------------------
 
-@pytest.mark.parametrize("d,D", [(1024, 16), (2048, 8), (4096, 4), (8192, 2)],
-                         ids=lambda v: str(v))
-def test_sweep_dt_sampled(d, D):
-    """Dyad-DT feed-forward at sweep shapes: fc1 d -> 4d, fc2 4d -> d (GELU' on fc2's dX), M = 16384."""
-    for li, (n_in, n_out, act) in enumerate(((d, 4 * d, "none"), (4 * d, d, "gelu"))):
-        banner("sweep", d, D, n_in, n_out)
-        check_full_layer(n_in, n_out, D, 16384, "DT", act, seed_offset=li)
+SWEEP_POINTS = [(d, D) for d in (1024, 2048, 4096, 8192) for D in (2, 4, 8, 16)]
+
+
+@pytest.mark.parametrize("layer", ["fc1", "fc2"])
+@pytest.mark.parametrize("d,D", SWEEP_POINTS, ids=lambda v: str(v))
+def test_sweep_dt_sampled(d, D, layer):
+    """Dyad-DT feed-forward at every width/block sweep point, M = 16384: fc1 d -> 4d (forward
+    with GELU and stash), fc2 4d -> d (input gradient with GELU'), each pass as benched."""
+    n_in, n_out = (d, 4 * d) if layer == "fc1" else (4 * d, d)
+    banner("sweep", d, D, layer)
+    fa, da = FF_ACTS[layer]
+    check_full_layer(n_in, n_out, D, 16384, "DT", fa, da, seed_offset=0 if layer == "fc1" else 1)
 
 
 @pytest.mark.parametrize("M", [16, 256, 32768])
@@ -399,7 +442,9 @@ def test_wide_it_forward(M):
     assert_close(y[rows], ref, "bf16", "Y rows")
 
 
-def test_wide_it_backward_sampled():
-    """Wide layer 8192 -> 32768, n_dyad 16, Dyad-IT dX and dW at M = 4096 tokens, sampled."""
-    banner("wide_backward")
-    check_full_layer(8192, 32768, 16, 4096, "IT", "none")
+@pytest.mark.parametrize("M", [4096, 32768])
+def test_wide_it_backward_sampled(M):
+    """Wide layer 8192 -> 32768, n_dyad 16, Dyad-IT forward, dX and dW, sampled; 32768 tokens
+    is the wide configuration's fwd+bwd batch."""
+    banner("wide_backward", M)
+    check_full_layer(8192, 32768, 16, M, "IT")

@@ -4,8 +4,9 @@ Each test fixes the oracle to an independent statement of the paper:
   * a dense weight assembled from ``scipy.linalg.block_diag`` (Sec. 2.2.1, Eq. 2)
     and the explicit permutation matrix P of Eq. 5 (Sec. 2.2.2), composed as the
     paper's Eq. 6 / Eq. 13 / Eq. 16 compose it;
-  * the paper's reshape/transpose/bmm formulation (Sec. 2.2-2.3) restated in
-    numpy, in the paper's feature-major layout;
+  * a gather / batched-product / scatter form built from the index definitions
+    (Eq. 3 and the strided view of Eq. 9 as explicit index arrays, the output
+    map of Sec. 2.4 as an explicit scatter);
   * special cases: n_dyad = 1 collapses to one dense matrix W1+W2; W2 = 0 gives a
     textbook batched GEMM; linearity;
   * structural counts: each component stores n_in*n_out/n_dyad distinct dense
@@ -79,29 +80,35 @@ def test_forward_matches_dense_through_permutation(variant, shape):
     np.testing.assert_allclose(Y, X @ W.T + b, rtol=1e-12, atol=1e-12)
 
 
-def paper_bmm_forward(variant, n_in, n_out, D, X, W1, W2, b):
-    """The paper's view/bmm formulation, feature-major (x is n_in x batch)."""
+def gathered_block_forward(variant, n_in, n_out, D, X, W1, W2, b):
+    """Forward from the definitions, in gather / batched-product / scatter form:
+    block i of component 1 reads input features i*bi + k (Eq. 3); component 2
+    reads features k*D + i under an input transpose (the strided view of Eq. 9,
+    as an explicit index array) and writes output j*D + i under an output
+    transpose (Sec. 2.4, as an explicit scatter), else i*bo + j."""
     bi, bo = n_in // D, n_out // D
-    x = X.T
-    x1 = x.reshape(D, bi, -1)                       # Eq. 3
-    x2 = x.reshape(bi, D, -1).transpose(1, 0, 2)    # Eq. 9
-    y1 = np.matmul(W1, x1).reshape(D * bo, -1)      # Eq. 4
-    if variant == "IT":
-        y2 = np.matmul(W2, x2).reshape(D * bo, -1)  # Eq. 10
-    elif variant == "OT":   # block product on the untransposed input, then the output transpose
-        y2 = np.matmul(W2, x1).transpose(1, 0, 2).reshape(bo * D, -1)
-    else:                   # both transposes
-        y2 = np.matmul(W2, x2).transpose(1, 0, 2).reshape(bo * D, -1)
-    return (y1 + y2 + b[:, None]).T
+    i_idx = np.arange(D)[:, None]
+    blk_in = i_idx * bi + np.arange(bi)[None, :]          # [D, bi]: i*bi + k
+    str_in = np.arange(bi)[None, :] * D + i_idx           # [D, bi]: k*D + i
+    blk_out = i_idx * bo + np.arange(bo)[None, :]         # [D, bo]: i*bo + j
+    str_out = np.arange(bo)[None, :] * D + i_idx          # [D, bo]: j*D + i
+    in2 = str_in if variant in ("IT", "DT") else blk_in
+    out2 = str_out if variant in ("OT", "DT") else blk_out
+    Y = np.tile(b, (X.shape[0], 1)).astype(np.float64)
+    for W, cols, rows in ((W1, blk_in, blk_out), (W2, in2, out2)):
+        G = X[:, cols]                                    # [M, D, bi] gathered input blocks
+        Z = np.einsum("ijk,mik->mij", W, G)               # [M, D, bo] block products
+        np.add.at(Y, (slice(None), rows), Z)              # scatter to the output features
+    return Y
 
 
 @pytest.mark.parametrize("variant", ["IT", "OT", "DT"])
 @pytest.mark.parametrize("shape", SHAPES)
-def test_forward_matches_paper_bmm_form(variant, shape):
+def test_forward_matches_gathered_block_form(variant, shape):
     n_in, n_out, D = shape
     X, W1, W2, b = rand_case(n_in, n_out, D, 6, 11)
     Y = oracle.forward(variant, n_in, n_out, D, X, W1, W2, b)
-    np.testing.assert_allclose(Y, paper_bmm_forward(variant, n_in, n_out, D, X, W1, W2, b),
+    np.testing.assert_allclose(Y, gathered_block_forward(variant, n_in, n_out, D, X, W1, W2, b),
                                rtol=1e-12, atol=1e-12)
 
 
