@@ -92,6 +92,27 @@ int dyad_forward(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dy
                  const void *bias, dyad_act act, void *Y, void *H, hipStream_t stream);
 
 /*
+ * dyad_forward for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.
+ * Same arguments, checks and results as dyad_forward (outputs within the
+ * same tolerance; the same plan, hence the same bits, whenever that plan's
+ * scratch fits).  It calls no hipMalloc, hipFree or allocating routine: where
+ * dyad_forward would take a split-reduction or large-batch buffer from its
+ * per-stream pool, this call takes it from a fixed static device array of
+ * 64 MiB (one per GPU the library runs on, held until the process ends; its
+ * address is looked up once per device).  A plan that would need more than
+ * 64 MiB of scratch is refused by the scratch array, and the call runs a plan
+ * that needs none.  No part of the array needs to start at zero: every plan
+ * writes each partial-sum slice in full before reading it.  All calls on one
+ * GPU share the one array: two calls whose work overlaps in time on that GPU
+ * (different streams, or different host threads without ordering) race and
+ * give undefined results; calls ordered on one stream are safe.
+ */
+int dyad_forward_noalloc(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                         dyad_dtype dtype, const void *X, const void *W1, const void *W2,
+                         const void *bias, dyad_act act, void *Y, void *H, hipStream_t stream);
+
+/*
  * Input gradient of y = W x + b (the paper gives no backward pass; this is the
  * gradient of Eq. 1): dX[m] = W^T dZ[m], where dZ is the gradient w.r.t. this
  * layer's linear output.  If this layer's input was X = GELU(H_in)

@@ -24,7 +24,7 @@ import torch  # loaded first: libdyad binds to the HIP runtime torch has loaded
 
 __all__ = [
     "IT", "OT", "DT", "F32", "BF16", "ACT_NONE", "ACT_GELU", "DyadError",
-    "dyad_forward", "dyad_backward_dx", "dyad_backward_dw", "dyad_dw_workspace_bytes",
+    "dyad_forward", "dyad_forward_noalloc", "dyad_backward_dx", "dyad_backward_dw", "dyad_dw_workspace_bytes",
     "dyad_strerror", "forward", "backward_dx", "backward_dw", "lib_path",
 ]
 
@@ -66,6 +66,8 @@ def _load():
     lib.dyad_forward.restype = _int
     lib.dyad_forward.argtypes = [_int, _i64, _i64, _i64, _i64, _int, _vp, _vp, _vp, _vp, _int,
                                  _vp, _vp, _vp]
+    lib.dyad_forward_noalloc.restype = _int
+    lib.dyad_forward_noalloc.argtypes = lib.dyad_forward.argtypes
     lib.dyad_backward_dx.restype = _int
     lib.dyad_backward_dx.argtypes = [_int, _i64, _i64, _i64, _i64, _int, _vp, _vp, _vp, _int,
                                      _vp, _vp, _vp]
@@ -85,6 +87,12 @@ def _load():
 def dyad_forward(variant, n_in, n_out, n_dyad, M, dtype, X, W1, W2, bias, act, Y, H, stream) -> int:
     return _load().dyad_forward(variant, n_in, n_out, n_dyad, M, dtype, X, W1, W2, bias, act, Y, H,
                                 stream)
+
+
+def dyad_forward_noalloc(variant, n_in, n_out, n_dyad, M, dtype, X, W1, W2, bias, act, Y, H,
+                         stream) -> int:
+    return _load().dyad_forward_noalloc(variant, n_in, n_out, n_dyad, M, dtype, X, W1, W2, bias, act,
+                                        Y, H, stream)
 
 
 def dyad_backward_dx(variant, n_in, n_out, n_dyad, M, dtype, dZ, W1, W2, act_in, H_in, dX,

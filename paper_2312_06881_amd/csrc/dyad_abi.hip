@@ -66,12 +66,11 @@ size_t dw_workspace(const DwPass &p) {
 
 }  // namespace
 
-extern "C" {
-
-int dyad_forward(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
-                 dyad_dtype dtype_arg, const void *X, const void *W1, const void *W2, const void *bias,
-                 dyad_act act_arg, void *Y, void *H, hipStream_t stream) {
-    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg), act = enum_value(act_arg);
+// dyad_forward and dyad_forward_noalloc: the same checks and plan; the
+// latter runs with the fixed scratch array in place of the stream's buffer.
+static int forward_impl(int variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M, int dtype,
+                        const void *X, const void *W1, const void *W2, const void *bias, int act, void *Y,
+                        void *H, hipStream_t stream, bool noalloc) {
     int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
     if (rc) return rc;
     if (act != DYAD_ACT_NONE && act != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
@@ -87,7 +86,30 @@ int dyad_forward(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t 
     p.dtype = dtype;
     p.epilogue = act == DYAD_ACT_GELU ? dyad::kEpiBiasGelu : dyad::kEpiBias;
     p.in = X; p.W1 = W1; p.W2 = W2; p.bias = bias; p.h_in = nullptr; p.out = Y; p.h_out = H;
+    if (!noalloc) return run_gemm(p, stream);
+    void *scr = nullptr;
+    if (dyad::noalloc_scratch(&scr) != hipSuccess) {
+        (void)hipGetLastError();
+        return DYAD_ERR_LAUNCH;
+    }
+    const dyad::ScratchScope scope(scr, dyad::kNoAllocScratchBytes);
     return run_gemm(p, stream);
+}
+
+extern "C" {
+
+int dyad_forward(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                 dyad_dtype dtype_arg, const void *X, const void *W1, const void *W2, const void *bias,
+                 dyad_act act_arg, void *Y, void *H, hipStream_t stream) {
+    return forward_impl(enum_value(variant_arg), n_in, n_out, n_dyad, M, enum_value(dtype_arg), X, W1, W2, bias,
+                        enum_value(act_arg), Y, H, stream, false);
+}
+
+int dyad_forward_noalloc(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                         dyad_dtype dtype_arg, const void *X, const void *W1, const void *W2, const void *bias,
+                         dyad_act act_arg, void *Y, void *H, hipStream_t stream) {
+    return forward_impl(enum_value(variant_arg), n_in, n_out, n_dyad, M, enum_value(dtype_arg), X, W1, W2, bias,
+                        enum_value(act_arg), Y, H, stream, true);
 }
 
 int dyad_backward_dx(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,

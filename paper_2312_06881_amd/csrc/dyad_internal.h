@@ -92,6 +92,25 @@ hipError_t launch_skinny_gemm(const GemmPass &p, hipStream_t s);
 // perm_last, the last slice holds block-order sums: output column j*D + g at
 // column g*bn + j).
 hipError_t split_workspace(hipStream_t s, size_t bytes, void **out);
+
+// dyad_forward_noalloc: while a ScratchScope lives on the calling thread,
+// split_workspace hands out its fixed buffer instead of the stream's pool
+// buffer, and refuses any request larger than it (the pass then takes a
+// plan that needs no buffer); it never allocates.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+struct ScratchScope {
+    void *ptr;
+    size_t bytes;
+    const ScratchScope *prev;
+    ScratchScope(void *p, size_t b);
+    ~ScratchScope();
+    ScratchScope(const ScratchScope &) = delete;
+    ScratchScope &operator=(const ScratchScope &) = delete;
+};
+const ScratchScope *current_scratch();
+// Device address of the fixed scratch array on the current device (looked up
+// once per device with hipGetSymbolAddress).
+hipError_t noalloc_scratch(void **out);
 hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s,
                                bool perm_last = false);
 

@@ -445,6 +445,12 @@ hipError_t pool_of(int dev, hipMemPool_t *out) {
 }  // namespace
 
 hipError_t split_workspace(hipStream_t s, size_t bytes, void **out) {
+    if (const ScratchScope *sc = current_scratch()) {
+        // the fixed scratch of dyad_forward_noalloc: never grown, never allocated
+        if (bytes > sc->bytes) return hipErrorOutOfMemory;
+        *out = sc->ptr;
+        return hipSuccess;
+    }
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;

@@ -16,10 +16,22 @@ int g_launches = 0;
 GemmPass g_gemm{};
 DwPass g_dw{};
 size_t g_dw_ws = 0;                 // what the mock workspace query reports
+const ScratchScope *g_scope = nullptr;       // innermost live ScratchScope
+bool g_seen_scope = false;           // a ScratchScope was in force at the last forward launch,
+void *g_seen_ptr = nullptr;          // with this buffer
+size_t g_seen_bytes = 0;             // of this size
 
 bool skinny_ok(const GemmPass &) { return false; }
 hipError_t launch_skinny_gemm(const GemmPass &, hipStream_t) { return hipErrorNotSupported; }
-hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t) { ++g_launches; g_gemm = p; return g_result; }
+hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t) {
+    ++g_launches;
+    g_gemm = p;
+    const ScratchScope *sc = current_scratch();
+    g_seen_scope = sc != nullptr;
+    g_seen_ptr = sc ? sc->ptr : nullptr;
+    g_seen_bytes = sc ? sc->bytes : 0;
+    return g_result;
+}
 hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t) { ++g_launches; g_gemm = p; return g_result; }
 hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t) { ++g_launches; g_gemm = p; return g_result; }
 bool mfma_dw_ok(const DwPass &) { return true; }
@@ -30,6 +42,12 @@ size_t simt_dw_workspace(const DwPass &) { return 0; }
 hipError_t launch_mfma_dw(const DwPass &p, hipStream_t) { ++g_launches; g_dw = p; return g_result; }
 hipError_t launch_general_mfma_dw(const DwPass &p, hipStream_t) { ++g_launches; g_dw = p; return g_result; }
 hipError_t launch_simt_dw(const DwPass &p, hipStream_t) { ++g_launches; g_dw = p; return g_result; }
+
+// the fixed scratch of dyad_forward_noalloc, mocked: a stand-in address
+ScratchScope::ScratchScope(void *p, size_t b) : ptr(p), bytes(b), prev(g_scope) { g_scope = this; }
+ScratchScope::~ScratchScope() { g_scope = prev; }
+const ScratchScope *current_scratch() { return g_scope; }
+hipError_t noalloc_scratch(void **out) { *out = (void *)0x400000; return hipSuccess; }
 
 }  // namespace dyad
 
@@ -67,6 +85,16 @@ int main() {
     // zero-padded widths: blocks are ceil(width / n_dyad)
     EXPECT(fwd(DYAD_OT, 7, 6, 2, 5, DYAD_F32, C, DYAD_ACT_NONE, C, nullptr) == DYAD_OK);
     EXPECT(g_gemm.bk == 4 && g_gemm.bn == 3);
+
+    // the no-allocation forward plans the same pass with the fixed scratch in scope
+    EXPECT(!g_seen_scope);
+    EXPECT(dyad_forward_noalloc(DYAD_DT, 768, 3072, 4, 100, DYAD_BF16, C, A, B, nullptr, DYAD_ACT_GELU, C, C,
+                                nullptr) == DYAD_OK);
+    EXPECT(g_seen_scope && g_seen_ptr == (void *)0x400000 && g_seen_bytes == kNoAllocScratchBytes);
+    EXPECT(current_scratch() == nullptr);
+    EXPECT(g_gemm.M == 100 && g_gemm.in_t && g_gemm.out_t && g_gemm.epilogue == kEpiBiasGelu);
+    EXPECT(dyad_forward_noalloc(DYAD_IT, 64, 256, 4, 8, (dyad_dtype)7, C, A, B, nullptr, DYAD_ACT_NONE, C,
+                                nullptr, nullptr) == DYAD_ERR_DTYPE);
 
     // a launch the runtime refuses is reported as DYAD_ERR_LAUNCH
     g_result = hipErrorLaunchFailure;
