@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--block", default="",
                     help="instead of the layer step: time an OPT-125m-shaped decoder block fwd+bwd "
                          "(dense, Dyad FF only, Dyad everywhere) with this variant (IT/OT/DT)")
+    ap.add_argument("--fused", action="store_true",
+                    help="feed-forward block with GELU inside fc2's kernels (fc1 writes only its "
+                         "pre-activation; dyad_forward_ex / dyad_backward_dw_ex)")
     ap.add_argument("--sets", type=int, default=0,
                     help="buffer sets to rotate (default: enough that a set recurs after ~512 MiB of traffic)")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("CALL", "FETCH_DIR", "WRITE_DIR"),
@@ -90,8 +93,10 @@ class Layer:
         self.flops = 4.0 * M * n_in * n_out / D
 
 
-def build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp):
-    """(name, flops, bytes, fn) for every C-ABI call of one step, in step order."""
+def build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp, fused=False):
+    """(name, flops, bytes, fn) for every C-ABI call of one step, in step order.  fused: the
+    feed-forward block with GELU inside fc2's kernels -- fc1 writes only its pre-activation
+    h, fc2's forward and weight gradient read h and apply GELU as they stage it."""
     D, M = wl.n_dyad, wl.M
     vid = {"IT": dy.IT, "OT": dy.OT, "DT": dy.DT}
 
@@ -102,6 +107,29 @@ def build_calls(dy, lib, wl, fc1, fc2, variants, ws, ws_bytes, sp):
     for v in variants:
         V = vid[v]
         ab = lambda kind, L, **kw: algorithmic_bytes(kind, L.n_in, L.n_out, D, M, **kw)  # noqa: E731
+        if fused:
+            out += [
+                (f"{v}:fc1.fwd", fc1.flops, ab("fwd", fc1),
+                 lambda V=V: lib.dyad_forward(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc1.X0), p(fc1.W1),
+                                              p(fc1.W2), p(fc1.b), dy.ACT_NONE, p(fc1.H), None, sp)),
+                (f"{v}:fc2.fwd", fc2.flops, ab("fwd", fc2),
+                 lambda V=V: lib.dyad_forward_ex(V, fc2.n_in, fc2.n_out, D, M, dy.BF16, dy.ACT_GELU, p(fc1.H),
+                                                 p(fc2.W1), p(fc2.W2), p(fc2.b), dy.ACT_NONE, p(fc2.Y), None, sp)),
+                (f"{v}:fc2.dx", fc2.flops, ab("dx", fc2, gelu=True),
+                 lambda V=V: lib.dyad_backward_dx(V, fc2.n_in, fc2.n_out, D, M, dy.BF16, p(fc2.dZ0),
+                                                  p(fc2.W1), p(fc2.W2), dy.ACT_GELU, p(fc1.H), p(fc2.dX), sp)),
+                (f"{v}:fc2.dw", fc2.flops, ab("dw", fc2),
+                 lambda V=V: lib.dyad_backward_dw_ex(V, fc2.n_in, fc2.n_out, D, M, dy.BF16, dy.ACT_GELU,
+                                                     p(fc2.dZ0), p(fc1.H), p(fc2.dW1), p(fc2.dW2), p(fc2.db),
+                                                     p(ws), ws_bytes, sp)),
+                (f"{v}:fc1.dx", fc1.flops, ab("dx", fc1),
+                 lambda V=V: lib.dyad_backward_dx(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc2.dX), p(fc1.W1),
+                                                  p(fc1.W2), dy.ACT_NONE, None, p(fc1.dX), sp)),
+                (f"{v}:fc1.dw", fc1.flops, ab("dw", fc1),
+                 lambda V=V: lib.dyad_backward_dw(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc2.dX), p(fc1.X0),
+                                                  p(fc1.dW1), p(fc1.dW2), p(fc1.db), p(ws), ws_bytes, sp)),
+            ]
+            continue
         out += [
             (f"{v}:fc1.fwd", fc1.flops, ab("fwd", fc1, stash=True),
              lambda V=V: lib.dyad_forward(V, fc1.n_in, fc1.n_out, D, M, dy.BF16, p(fc1.X0), p(fc1.W1),
@@ -246,15 +274,15 @@ def main():
         n_sets = args.sets
     layers = [(Layer(torch, i1, o1, D, M, 0, dev), Layer(torch, i2, o2, D, M, 1, dev)) for _ in range(n_sets)]
     fc1, fc2 = layers[0]
-    ws_bytes = max(dy.dyad_dw_workspace_bytes(vid[v], L.n_in, L.n_out, D, M, dy.BF16)
-                   for v in variants for L in (fc1, fc2))
+    ws_bytes = max(dy.dyad_dw_workspace_bytes_ex(vid[v], L.n_in, L.n_out, D, M, dy.BF16, a)
+                   for v in variants for L in (fc1, fc2) for a in (dy.ACT_NONE, dy.ACT_GELU))
     ws = torch.empty((max(ws_bytes, 16),), dtype=torch.uint8, device=dev)
 
     def check(rc):
         if rc != 0:
             raise RuntimeError(dy.dyad_strerror(rc))
 
-    sets = [build_calls(dy, lib, wl, a, b, variants, ws, ws_bytes, sp) for a, b in layers]
+    sets = [build_calls(dy, lib, wl, a, b, variants, ws, ws_bytes, sp, args.fused) for a, b in layers]
     calls = sets[0]
     n_calls = len(calls)
     if args.only:
@@ -365,8 +393,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.note, "n_dyad": D, "tokens": M,
                    "layers": [list(l) for l in wl.layers], "variants": variants,
-                   "step": "per variant: fc1 fwd(GELU, stash) + fc2 fwd + fc2 dX(GELU') + fc2 dW+db "
-                           "+ fc1 dX + fc1 dW+db",
+                   "step": ("per variant: fc1 fwd (pre-activation only) + fc2 fwd (GELU on load) + "
+                            "fc2 dX(GELU') + fc2 dW+db (GELU on load) + fc1 dX + fc1 dW+db") if args.fused else
+                           ("per variant: fc1 fwd(GELU, stash) + fc2 fwd + fc2 dX(GELU') + fc2 dW+db "
+                            "+ fc1 dX + fc1 dW+db"),
+                   "fused_ff": bool(args.fused),
                    "buffer_sets": n_sets},
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "per_variant": per_variant,

@@ -72,7 +72,7 @@ typedef enum { DYAD_ACT_NONE = 0, DYAD_ACT_GELU = 1 } dyad_act; /* GELU(x) = x *
 typedef enum {
     DYAD_OK = 0,
     DYAD_ERR_INVALID_ARG = -1, /* unknown enum, size < 0 (M) or <= 0 (n_in, n_out, n_dyad), size overflow, NULL required pointer */
-    DYAD_ERR_SHAPE = -2,       /* reserved: every shape is accepted (widths n_dyad does not divide are zero-padded) */
+    DYAD_ERR_SHAPE = -2,       /* only the _ex calls with an input activation: no kernel for this shape */
     DYAD_ERR_ALIGN = -3,       /* a non-NULL pointer is not 16-byte aligned */
     DYAD_ERR_DTYPE = -4,       /* unknown dtype */
     DYAD_ERR_WORKSPACE = -5,   /* dW workspace NULL or smaller than dyad_dw_workspace_bytes() */
@@ -113,6 +113,25 @@ int dyad_forward_noalloc(dyad_variant variant, int64_t n_in, int64_t n_out, int6
                          const void *bias, dyad_act act, void *Y, void *H, hipStream_t stream);
 
 /*
+ * dyad_forward for a layer whose input is an activation of X: with
+ * act_in == DYAD_ACT_GELU it computes Y = W GELU(X) + bias (then act and H as
+ * in dyad_forward), where X is the stashed pre-activation of the layer before
+ * (the H that dyad_forward wrote for it) -- the second layer of a feed-forward
+ * block fc1 -> GELU -> fc2 whose activation is never written to memory
+ * (the paper times that block as one unit, Sec. 3.3; the concatenated-component
+ * idea of Sec. 3.4.3 is carried further by fusing the activation too).  GELU
+ * is applied to the input operand as it is staged, in fp32, rounded once to
+ * bf16.  act_in == DYAD_ACT_NONE is exactly dyad_forward.  With GELU it runs
+ * on the matrix-core tiles only: bf16 (else DYAD_ERR_DTYPE), n_dyad in
+ * {1, 2, 4, 8, 16} dividing both widths, input blocks a multiple of 32, output
+ * blocks a multiple of 64, and no output transpose (Dyad-OT / -DT) above
+ * n_dyad 4; any other shape returns DYAD_ERR_SHAPE before any launch.
+ */
+int dyad_forward_ex(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                    dyad_dtype dtype, dyad_act act_in, const void *X, const void *W1, const void *W2,
+                    const void *bias, dyad_act act, void *Y, void *H, hipStream_t stream);
+
+/*
  * Input gradient of y = W x + b (the paper gives no backward pass; this is the
  * gradient of Eq. 1): dX[m] = W^T dZ[m], where dZ is the gradient w.r.t. this
  * layer's linear output.  If this layer's input was X = GELU(H_in)
@@ -139,6 +158,24 @@ int dyad_backward_dw(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t 
 /* Workspace bytes dyad_backward_dw needs for these arguments (0 if none, or if they are invalid). */
 size_t dyad_dw_workspace_bytes(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad,
                                int64_t M, dyad_dtype dtype);
+
+/*
+ * Weight and bias gradients of the layer of dyad_forward_ex: with
+ * act_in == DYAD_ACT_GELU the layer's input is GELU(X), X the stashed
+ * pre-activation, formed as X is staged (dW_c[i][j][k] = sum_m dZ[m][row]
+ * GELU(X[m][col])); db as in dyad_backward_dw.  act_in == DYAD_ACT_NONE is
+ * exactly dyad_backward_dw.  With GELU: bf16 (else DYAD_ERR_DTYPE), n_dyad in
+ * {1, 2, 4, 8, 16} dividing both widths into blocks of multiples of 64, else
+ * DYAD_ERR_SHAPE before any launch.  workspace must hold
+ * dyad_dw_workspace_bytes_ex() bytes for the same arguments.
+ */
+int dyad_backward_dw_ex(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                        dyad_dtype dtype, dyad_act act_in, const void *dZ, const void *X, void *dW1, void *dW2,
+                        void *dbias, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes dyad_backward_dw_ex needs (0 if none, or if the arguments are invalid or unsupported). */
+size_t dyad_dw_workspace_bytes_ex(dyad_variant variant, int64_t n_in, int64_t n_out, int64_t n_dyad,
+                                  int64_t M, dyad_dtype dtype, dyad_act act_in);
 
 /* Static, human-readable text for a dyad_status value. */
 const char *dyad_strerror(int status);

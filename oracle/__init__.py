@@ -53,6 +53,8 @@ def _load():
     lib.oracle_gelu_grad.restype = ctypes.c_double
     lib.oracle_gelu_grad.argtypes = [ctypes.c_double]
     lib.oracle_threads.restype = ctypes.c_int
+    lib.oracle_gelu_vec.restype = None
+    lib.oracle_gelu_vec.argtypes = [_I64, _D, _D]
     lib.oracle_forward.restype = None
     lib.oracle_forward.argtypes = [ctypes.c_int, _I64, _I64, _I64, _I64,
                                    _D, _D, _D, _D, ctypes.c_int, _D, _D]
@@ -105,6 +107,15 @@ def gelu(x: float) -> float:
 
 def gelu_grad(x: float) -> float:
     return _load().oracle_gelu_grad(float(x))
+
+
+def gelu_array(x):
+    """GELU(x) = x Phi(x) elementwise, fp64, any shape."""
+    lib = _load()
+    x = _f64(x)
+    out = np.empty_like(x)
+    lib.oracle_gelu_vec(x.size, _ptr(x), _ptr(out))
+    return out
 
 
 def threads() -> int:

@@ -92,6 +92,16 @@ double oracle_gelu_grad(double x)
     return normal_cdf(x) + x * exp(-0.5 * x * x) / sqrt(2.0 * pi);
 }
 
+/* out[e] = GELU(in[e]) for n values: the activated input of a layer that
+ * follows a GELU (fc2 of a feed-forward block), formed elementwise. */
+void oracle_gelu_vec(int64_t n, const double *in, double *out)
+{
+    int64_t e;
+#pragma omp parallel for schedule(static)
+    for (e = 0; e < n; ++e)
+        out[e] = oracle_gelu(in[e]);
+}
+
 int oracle_threads(void)
 {
     return omp_get_max_threads();

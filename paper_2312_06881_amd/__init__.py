@@ -24,7 +24,8 @@ import torch  # loaded first: libdyad binds to the HIP runtime torch has loaded
 
 __all__ = [
     "IT", "OT", "DT", "F32", "BF16", "ACT_NONE", "ACT_GELU", "DyadError",
-    "dyad_forward", "dyad_forward_noalloc", "dyad_backward_dx", "dyad_backward_dw", "dyad_dw_workspace_bytes",
+    "dyad_forward", "dyad_forward_noalloc", "dyad_forward_ex", "dyad_backward_dx", "dyad_backward_dw",
+    "dyad_backward_dw_ex", "dyad_dw_workspace_bytes", "dyad_dw_workspace_bytes_ex",
     "dyad_strerror", "forward", "backward_dx", "backward_dw", "lib_path",
 ]
 
@@ -76,6 +77,14 @@ def _load():
                                      _vp, ctypes.c_size_t, _vp]
     lib.dyad_dw_workspace_bytes.restype = ctypes.c_size_t
     lib.dyad_dw_workspace_bytes.argtypes = [_int, _i64, _i64, _i64, _i64, _int]
+    lib.dyad_forward_ex.restype = _int
+    lib.dyad_forward_ex.argtypes = [_int, _i64, _i64, _i64, _i64, _int, _int, _vp, _vp, _vp, _vp, _int,
+                                    _vp, _vp, _vp]
+    lib.dyad_backward_dw_ex.restype = _int
+    lib.dyad_backward_dw_ex.argtypes = [_int, _i64, _i64, _i64, _i64, _int, _int, _vp, _vp, _vp, _vp, _vp,
+                                        _vp, ctypes.c_size_t, _vp]
+    lib.dyad_dw_workspace_bytes_ex.restype = ctypes.c_size_t
+    lib.dyad_dw_workspace_bytes_ex.argtypes = [_int, _i64, _i64, _i64, _i64, _int, _int]
     lib.dyad_strerror.restype = ctypes.c_char_p
     lib.dyad_strerror.argtypes = [_int]
     _lib = lib
@@ -95,6 +104,12 @@ def dyad_forward_noalloc(variant, n_in, n_out, n_dyad, M, dtype, X, W1, W2, bias
                                         Y, H, stream)
 
 
+def dyad_forward_ex(variant, n_in, n_out, n_dyad, M, dtype, act_in, X, W1, W2, bias, act, Y, H,
+                    stream) -> int:
+    return _load().dyad_forward_ex(variant, n_in, n_out, n_dyad, M, dtype, act_in, X, W1, W2, bias, act,
+                                   Y, H, stream)
+
+
 def dyad_backward_dx(variant, n_in, n_out, n_dyad, M, dtype, dZ, W1, W2, act_in, H_in, dX,
                      stream) -> int:
     return _load().dyad_backward_dx(variant, n_in, n_out, n_dyad, M, dtype, dZ, W1, W2, act_in,
@@ -109,6 +124,16 @@ def dyad_backward_dw(variant, n_in, n_out, n_dyad, M, dtype, dZ, X, dW1, dW2, db
 
 def dyad_dw_workspace_bytes(variant, n_in, n_out, n_dyad, M, dtype) -> int:
     return _load().dyad_dw_workspace_bytes(variant, n_in, n_out, n_dyad, M, dtype)
+
+
+def dyad_backward_dw_ex(variant, n_in, n_out, n_dyad, M, dtype, act_in, dZ, X, dW1, dW2, dbias, workspace,
+                        workspace_bytes, stream) -> int:
+    return _load().dyad_backward_dw_ex(variant, n_in, n_out, n_dyad, M, dtype, act_in, dZ, X, dW1, dW2,
+                                       dbias, workspace, workspace_bytes, stream)
+
+
+def dyad_dw_workspace_bytes_ex(variant, n_in, n_out, n_dyad, M, dtype, act_in) -> int:
+    return _load().dyad_dw_workspace_bytes_ex(variant, n_in, n_out, n_dyad, M, dtype, act_in)
 
 
 def dyad_strerror(status: int) -> str:
@@ -163,12 +188,13 @@ def _width(n, D, b, what):
     return n
 
 
-def forward(x, w1, w2, bias=None, variant="IT", act="none", stash_h=False, n_out=None):
+def forward(x, w1, w2, bias=None, variant="IT", act="none", stash_h=False, n_out=None, act_in="none"):
     """y = W x + b per token (optionally GELU); returns y, or (y, h) with the pre-activation h.
 
     Weights are [n_dyad, bo, bi]; x is [M, n_in] with n_in padded up to n_dyad * bi.  n_out
     defaults to n_dyad * bo (or bias's length); a smaller n_out needing the same bo blocks is
-    a zero-padded layer."""
+    a zero-padded layer.  act_in="gelu": the layer's input is GELU(x), x being the previous
+    layer's pre-activation, applied inside the kernel (dyad_forward_ex)."""
     D, bo, bi = w1.shape
     M, n_in = x.shape
     _width(n_in, D, bi, "n_in")
@@ -176,8 +202,13 @@ def forward(x, w1, w2, bias=None, variant="IT", act="none", stash_h=False, n_out
     a = _act(act)
     y = torch.empty((M, n_out), dtype=x.dtype, device=x.device)
     h = torch.empty_like(y) if (stash_h and a == ACT_GELU) else None
-    _check(dyad_forward(_variant(variant), n_in, n_out, D, M, _dtype(x, w1, w2, bias), _ptr(x),
-                        _ptr(w1), _ptr(w2), _ptr(bias), a, _ptr(y), _ptr(h), _stream(x)))
+    ai = _act(act_in)
+    if ai == ACT_NONE:
+        _check(dyad_forward(_variant(variant), n_in, n_out, D, M, _dtype(x, w1, w2, bias), _ptr(x),
+                            _ptr(w1), _ptr(w2), _ptr(bias), a, _ptr(y), _ptr(h), _stream(x)))
+    else:
+        _check(dyad_forward_ex(_variant(variant), n_in, n_out, D, M, _dtype(x, w1, w2, bias), ai, _ptr(x),
+                               _ptr(w1), _ptr(w2), _ptr(bias), a, _ptr(y), _ptr(h), _stream(x)))
     return (y, h) if stash_h else y
 
 
@@ -195,8 +226,9 @@ def backward_dx(dz, w1, w2, variant="IT", act_in="none", h_in=None, n_in=None):
     return dx
 
 
-def backward_dw(dz, x, n_dyad, variant="IT", want_db=True, workspace=None):
-    """(dW1, dW2, db) of one layer; db is None unless want_db."""
+def backward_dw(dz, x, n_dyad, variant="IT", want_db=True, workspace=None, act_in="none"):
+    """(dW1, dW2, db) of one layer; db is None unless want_db.  act_in="gelu": the layer's
+    input is GELU(x), formed inside the kernel (dyad_backward_dw_ex)."""
     M, n_out = dz.shape
     n_in = x.shape[1]
     D = n_dyad
@@ -206,10 +238,11 @@ def backward_dw(dz, x, n_dyad, variant="IT", want_db=True, workspace=None):
     dw2 = torch.empty(shp, dtype=dz.dtype, device=dz.device)
     db = torch.empty((n_out,), dtype=dz.dtype, device=dz.device) if want_db else None
     v = _variant(variant)
-    need = dyad_dw_workspace_bytes(v, n_in, n_out, D, M, dt)
+    ai = _act(act_in)
+    need = dyad_dw_workspace_bytes_ex(v, n_in, n_out, D, M, dt, ai)
     if workspace is None and need:
         workspace = torch.empty((need,), dtype=torch.uint8, device=dz.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(dyad_backward_dw(v, n_in, n_out, D, M, dt, _ptr(dz), _ptr(x), _ptr(dw1), _ptr(dw2),
-                            _ptr(db), _ptr(workspace), ws_bytes, _stream(dz)))
+    _check(dyad_backward_dw_ex(v, n_in, n_out, D, M, dt, ai, _ptr(dz), _ptr(x), _ptr(dw1), _ptr(dw2),
+                               _ptr(db), _ptr(workspace), ws_bytes, _stream(dz)))
     return dw1, dw2, db

@@ -176,7 +176,9 @@ struct DwSlots {
 // pipelined loop would also issue the loads of four stages that read only
 // zeros, and at 16 tokens those loads, not the stores, set the time.  Its own
 // kernel instance, so the pipelined kernel's registers are unaffected.
-template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool C2, bool MG, bool ONE>
+// XG: the layer's input is GELU(X) (a layer after a GELU, given the stashed
+// pre-activation): the activation is applied to the X operand as it is staged.
+template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool C2, bool MG, bool ONE, bool XG>
 __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, int split, int g, int jt, int kt) {
     using C = DwCfg<BJ, BK, WJN, WKN>;
     constexpr int GB = MG ? mg_gb<D, BJ, BK, WJN, WKN>() : 1;
@@ -264,13 +266,18 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         fetch_side(SB{}, sb, set, buffer_rsrc((C2 ? a.X2 : a.X) + base * a.n_in, rows * n_in * 2u), rows);
     };
     // ---- registers -> LDS stage buffer
-    auto stash_side = [&](auto side, auto swz, auto &sl, auto set, unsigned char *buf) {
+    auto stash_side = [&](auto side, auto swz, auto &sl, auto set, unsigned char *buf, auto xg) {
         using S = decltype(side);
         constexpr bool SWZ = decltype(swz)::value;
         constexpr int P = decltype(set)::value;
         constexpr int W = S::kKind == 2 ? S::kPerRow * S::kNJ : 0;
 #pragma unroll
         for (int q = 0; q < S::kSlots; ++q) {
+            if constexpr (decltype(xg)::value) {
+                // GELU(X): every loaded value feeds some group, so whole vectors are activated
+#pragma unroll
+                for (int v = 0; v < (S::kKind == 1 ? 1 : S::kVec); ++v) sl.r[P][q][v] = gelu8(sl.r[P][q][v]);
+            }
             if (S::kItems % T == 0 || sl.ok[q]) {
                 if constexpr (S::kKind == 2) stash_pieces<D, S::kNJ, SWZ>(sl.r[P][q], buf + sl.lo[q], sl.sw[q], sl.lb[q], 2 * W);
                 else *reinterpret_cast<uint4 *>(buf + sl.lo[q]) = sl.r[P][q][0];
@@ -278,8 +285,8 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
         }
     };
     auto stash = [&](auto set, unsigned char *buf) {
-        stash_side(SA{}, std::bool_constant<L::kSwzA>{}, sa, set, buf);
-        stash_side(SB{}, std::bool_constant<L::kSwzB>{}, sb, set, buf);
+        stash_side(SA{}, std::bool_constant<L::kSwzA>{}, sa, set, buf, std::false_type{});
+        stash_side(SB{}, std::bool_constant<L::kSwzB>{}, sb, set, buf, std::bool_constant<XG>{});
     };
 
     f32x4_t acc[C::kSubJ][C::kSubK];
@@ -425,7 +432,7 @@ struct DwKernel {
     static_assert(kLds >= C::kWaves * 16 * C::WK * 2, "the direct epilogue's slices fit the stage buffers");
 };
 
-template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool ONE>
+template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool ONE, bool XG = false>
 __global__ void __launch_bounds__(64 * WJN * WKN, (DwCfg<BJ, BK, WJN, WKN>::kMinBlocks))
 dyad_dw_mfma(DwArgs a) {
     using K = DwKernel<D, BJ, BK, WJN, WKN, IN_T, OUT_T>;
@@ -440,12 +447,12 @@ dyad_dw_mfma(DwArgs a) {
         const int kt = t % a.tiles_k;
         const int jt = (t / a.tiles_k) % a.tiles_j;
         const int g = t / (a.tiles_k * a.tiles_j);
-        if (comp == 0) dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false, false, ONE>(a, smem, split, g, jt, kt);
-        else dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, false, ONE>(a, smem, split, g, jt, kt);
+        if (comp == 0) dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false, false, ONE, XG>(a, smem, split, g, jt, kt);
+        else dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, false, ONE, XG>(a, smem, split, g, jt, kt);
     } else if constexpr (K::kMG) {
         // all groups: (D / GB) * tiles_j x GB * tiles_k tiles of (BJ / GA) x (BK / GB)
         const int nk = K::kGB * a.tiles_k;
-        dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, true, ONE>(a, smem, split, 0, t / nk, t % nk);
+        dw_tile<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, true, ONE, XG>(a, smem, split, 0, t / nk, t % nk);
     }
 }
 
@@ -459,7 +466,7 @@ struct DwPlan {
 };
 
 // Launches the weight-gradient kernel of plan `pl` and the split reduction.
-template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T>
+template <int D, int BJ, int BK, int WJN, int WKN, bool IN_T, bool OUT_T, bool XG = false>
 hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     using C = DwCfg<BJ, BK, WJN, WKN>;
     DwArgs a;
@@ -480,9 +487,9 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.items = pl.splits * 2 * D * pl.tiles_j * pl.tiles_k;
     a.want_db = p.db != nullptr;
     if (pl.tokens_per_split >= p.M && p.M <= kStageK)   // one split of one stage
-        dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
+        dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, XG><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
     else
-        dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
+        dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, false, XG><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.direct) return e;
     const int64_t per_comp = p.D * p.bo * p.bi;
@@ -532,16 +539,20 @@ hipError_t launch_dw_plain(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_it(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_ot(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_dt(const DwPass &p, const DwPlan &pl, hipStream_t s);
+// the same with X = GELU(X as passed) (DwPass::gelu_x)
+hipError_t launch_dw_xg_it(const DwPass &p, const DwPlan &pl, hipStream_t s);
+hipError_t launch_dw_xg_ot(const DwPass &p, const DwPlan &pl, hipStream_t s);
+hipError_t launch_dw_xg_dt(const DwPass &p, const DwPlan &pl, hipStream_t s);
 
-template <bool IN_T, bool OUT_T>
+template <bool IN_T, bool OUT_T, bool XG = false>
 hipError_t launch_dw_variant(const DwPass &p, const DwPlan &pl, hipStream_t s) {
 #define DYAD_DW_CASE(J_, K_, WJ_, WK_)                                                      \
     if (pl.BJ == J_ && pl.BK == K_ && pl.WJN == WJ_ && pl.WKN == WK_) switch (p.D) {        \
-        case 1: return launch_dw_cfg<1, J_, K_, WJ_, WK_, IN_T, OUT_T>(p, pl, s);           \
-        case 2: return launch_dw_cfg<2, J_, K_, WJ_, WK_, IN_T, OUT_T>(p, pl, s);           \
-        case 4: return launch_dw_cfg<4, J_, K_, WJ_, WK_, IN_T, OUT_T>(p, pl, s);           \
-        case 8: return launch_dw_cfg<8, J_, K_, WJ_, WK_, IN_T, OUT_T>(p, pl, s);           \
-        case 16: return launch_dw_cfg<16, J_, K_, WJ_, WK_, IN_T, OUT_T>(p, pl, s);         \
+        case 1: return launch_dw_cfg<1, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
+        case 2: return launch_dw_cfg<2, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
+        case 4: return launch_dw_cfg<4, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
+        case 8: return launch_dw_cfg<8, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
+        case 16: return launch_dw_cfg<16, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);     \
         default: return hipErrorNotSupported;                                               \
     }
     DYAD_DW_CONFIGS(DYAD_DW_CASE)

@@ -101,9 +101,11 @@ bool dw_permuted(const DwPass &p) {
 }
 
 // The plan a pass runs with (for the permuted form, that of plain operands).
+// With GELU(X) the fused form always runs: the activation is applied where X
+// is staged, which the block-ordered copies would bypass.
 bool plan(const DwPass &p, DwPlan &pl, bool *permuted) {
     *permuted = false;
-    if (dw_permuted(p)) {
+    if (!p.gelu_x && dw_permuted(p)) {
         DwPass q = p;
         q.in_t = q.out_t = false;
         if (choose(q, pl)) {
@@ -170,6 +172,12 @@ hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s) {
             q.X2 = x2;
         }
         return e == hipSuccess ? launch_dw_plain(q, pl, s) : e;
+    }
+    if (p.gelu_x) {
+        if (p.in_t && !p.out_t) return launch_dw_xg_it(p, pl, s);
+        if (!p.in_t && p.out_t) return launch_dw_xg_ot(p, pl, s);
+        if (p.in_t && p.out_t) return launch_dw_xg_dt(p, pl, s);
+        return hipErrorNotSupported;
     }
     if (p.in_t && !p.out_t) return launch_dw_it(p, pl, s);
     if (!p.in_t && p.out_t) return launch_dw_ot(p, pl, s);

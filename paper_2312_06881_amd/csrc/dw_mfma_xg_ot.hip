@@ -1,0 +1,11 @@
+// Weight-gradient kernels of Dyad-OT for a layer whose input is GELU(X), the
+// activation applied to X as it is staged; every tile configuration and n_dyad.
+#include "dw_mfma.h"
+
+namespace dyad {
+
+hipError_t launch_dw_xg_ot(const DwPass &p, const DwPlan &pl, hipStream_t s) {
+    return launch_dw_variant<false, true, true>(p, pl, s);
+}
+
+}  // namespace dyad

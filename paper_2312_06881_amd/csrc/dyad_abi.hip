@@ -70,10 +70,12 @@ size_t dw_workspace(const DwPass &p) {
 // latter runs with the fixed scratch array in place of the stream's buffer.
 static int forward_impl(int variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M, int dtype,
                         const void *X, const void *W1, const void *W2, const void *bias, int act, void *Y,
-                        void *H, hipStream_t stream, bool noalloc) {
+                        void *H, hipStream_t stream, bool noalloc, int act_in = DYAD_ACT_NONE) {
     int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
     if (rc) return rc;
     if (act != DYAD_ACT_NONE && act != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
+    if (act_in != DYAD_ACT_NONE && act_in != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
+    if (act_in == DYAD_ACT_GELU && dtype != DYAD_BF16) return DYAD_ERR_DTYPE;
     if (!W1 || !W2 || (M > 0 && (!X || !Y))) return DYAD_ERR_INVALID_ARG;
     if (act == DYAD_ACT_NONE) H = nullptr;
     if (!aligned16(X) || !aligned16(W1) || !aligned16(W2) || !aligned16(bias) || !aligned16(Y) ||
@@ -86,6 +88,12 @@ static int forward_impl(int variant, int64_t n_in, int64_t n_out, int64_t n_dyad
     p.dtype = dtype;
     p.epilogue = act == DYAD_ACT_GELU ? dyad::kEpiBiasGelu : dyad::kEpiBias;
     p.in = X; p.W1 = W1; p.W2 = W2; p.bias = bias; p.h_in = nullptr; p.out = Y; p.h_out = H;
+    if (act_in == DYAD_ACT_GELU) {
+        // only the matrix-core tiles apply an input activation; other shapes are refused
+        p.gelu_in = true;
+        const hipError_t e = dyad::launch_mfma_gemm(p, stream);
+        return e == hipErrorNotSupported ? DYAD_ERR_SHAPE : launch_status(e);
+    }
     if (!noalloc) return run_gemm(p, stream);
     void *scr = nullptr;
     if (dyad::noalloc_scratch(&scr) != hipSuccess) {
@@ -103,6 +111,13 @@ int dyad_forward(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t 
                  dyad_act act_arg, void *Y, void *H, hipStream_t stream) {
     return forward_impl(enum_value(variant_arg), n_in, n_out, n_dyad, M, enum_value(dtype_arg), X, W1, W2, bias,
                         enum_value(act_arg), Y, H, stream, false);
+}
+
+int dyad_forward_ex(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                    dyad_dtype dtype_arg, dyad_act act_in_arg, const void *X, const void *W1, const void *W2,
+                    const void *bias, dyad_act act_arg, void *Y, void *H, hipStream_t stream) {
+    return forward_impl(enum_value(variant_arg), n_in, n_out, n_dyad, M, enum_value(dtype_arg), X, W1, W2, bias,
+                        enum_value(act_arg), Y, H, stream, false, enum_value(act_in_arg));
 }
 
 int dyad_forward_noalloc(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
@@ -148,17 +163,33 @@ size_t dyad_dw_workspace_bytes(dyad_variant variant_arg, int64_t n_in, int64_t n
     return dw_workspace(make_dw(variant, n_in, n_out, n_dyad, M, dtype));
 }
 
-int dyad_backward_dw(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
-                     dyad_dtype dtype_arg, const void *dZ, const void *X, void *dW1, void *dW2, void *dbias,
-                     void *workspace, size_t workspace_bytes, hipStream_t stream) {
-    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg);
+size_t dyad_dw_workspace_bytes_ex(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad,
+                                  int64_t M, dyad_dtype dtype_arg, dyad_act act_in_arg) {
+    const int variant = enum_value(variant_arg), dtype = enum_value(dtype_arg), act_in = enum_value(act_in_arg);
+    if (check_sizes(variant, n_in, n_out, n_dyad, M, dtype)) return 0;
+    if (act_in == DYAD_ACT_NONE) return dw_workspace(make_dw(variant, n_in, n_out, n_dyad, M, dtype));
+    if (act_in != DYAD_ACT_GELU || dtype != DYAD_BF16) return 0;
+    DwPass p = make_dw(variant, n_in, n_out, n_dyad, M, dtype);
+    p.gelu_x = true;
+    return dyad::mfma_dw_ok(p) ? dyad::mfma_dw_workspace(p) : 0;
+}
+
+static int backward_dw_impl(int variant, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M, int dtype,
+                            int act_in, const void *dZ, const void *X, void *dW1, void *dW2, void *dbias,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream) {
     int rc = check_sizes(variant, n_in, n_out, n_dyad, M, dtype);
     if (rc) return rc;
+    if (act_in != DYAD_ACT_NONE && act_in != DYAD_ACT_GELU) return DYAD_ERR_INVALID_ARG;
+    if (act_in == DYAD_ACT_GELU && dtype != DYAD_BF16) return DYAD_ERR_DTYPE;
     if (!dW1 || !dW2 || (M > 0 && (!dZ || !X))) return DYAD_ERR_INVALID_ARG;
     if (!aligned16(dZ) || !aligned16(X) || !aligned16(dW1) || !aligned16(dW2) || !aligned16(dbias) ||
         !aligned16(workspace))
         return DYAD_ERR_ALIGN;
     DwPass p = make_dw(variant, n_in, n_out, n_dyad, M, dtype);
+    p.gelu_x = act_in == DYAD_ACT_GELU;
+    // an input activation runs on the matrix-core kernels only (an empty batch
+    // has nothing to activate and takes the usual zero-gradient path)
+    if (p.gelu_x && M > 0 && !dyad::mfma_dw_ok(p)) return DYAD_ERR_SHAPE;
     size_t need = dw_workspace(p);
     if (need > 0 && (!workspace || workspace_bytes < need)) return DYAD_ERR_WORKSPACE;
     p.dZ = dZ; p.X = X; p.dW1 = dW1; p.dW2 = dW2; p.db = dbias; p.ws = workspace; p.ws_bytes = workspace_bytes;
@@ -168,11 +199,25 @@ int dyad_backward_dw(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int6
     return launch_status(e);
 }
 
+int dyad_backward_dw(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                     dyad_dtype dtype_arg, const void *dZ, const void *X, void *dW1, void *dW2, void *dbias,
+                     void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    return backward_dw_impl(enum_value(variant_arg), n_in, n_out, n_dyad, M, enum_value(dtype_arg), DYAD_ACT_NONE,
+                            dZ, X, dW1, dW2, dbias, workspace, workspace_bytes, stream);
+}
+
+int dyad_backward_dw_ex(dyad_variant variant_arg, int64_t n_in, int64_t n_out, int64_t n_dyad, int64_t M,
+                        dyad_dtype dtype_arg, dyad_act act_in_arg, const void *dZ, const void *X, void *dW1,
+                        void *dW2, void *dbias, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    return backward_dw_impl(enum_value(variant_arg), n_in, n_out, n_dyad, M, enum_value(dtype_arg),
+                            enum_value(act_in_arg), dZ, X, dW1, dW2, dbias, workspace, workspace_bytes, stream);
+}
+
 const char *dyad_strerror(int status) {
     switch (status) {
     case DYAD_OK: return "ok";
     case DYAD_ERR_INVALID_ARG: return "invalid argument (enum, size or NULL pointer)";
-    case DYAD_ERR_SHAPE: return "unsupported shape";
+    case DYAD_ERR_SHAPE: return "no kernel applies an input activation to this shape";
     case DYAD_ERR_ALIGN: return "pointer not 16-byte aligned";
     case DYAD_ERR_DTYPE: return "unsupported dtype";
     case DYAD_ERR_WORKSPACE: return "dW workspace missing or too small";

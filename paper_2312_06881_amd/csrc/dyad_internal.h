@@ -34,6 +34,7 @@ enum Epilogue {
 struct GemmPass {
     int64_t M, Kin, Nout, D, bk, bn;
     bool in_t, out_t, w_t;
+    bool gelu_in;    // forward only: the input operand is GELU(in), formed as it is staged
     int dtype;       // Dtype
     int epilogue;    // Epilogue
     const void *in, *W1, *W2, *bias, *h_in;
@@ -50,6 +51,7 @@ struct DwPass {
     bool in_t, out_t;
     int dtype;
     const void *dZ, *X;
+    bool gelu_x;     // X is GELU(X as passed), formed as it is staged
     void *dW1, *dW2, *db;
     void *ws;
     size_t ws_bytes;

@@ -82,7 +82,11 @@ struct GemmCfg {
     static_assert(kLds <= 160 * 1024, "LDS budget");
 };
 
-template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int OCC, int PF = 1>
+// GELU_IN: the pass's input is GELU(in) (a layer after a GELU, fed the
+// stashed pre-activation): the activation is applied to the input operand as
+// it is staged into LDS, so the activated tensor never exists in HBM.
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int OCC, int PF = 1,
+          bool GELU_IN = false>
 __global__ void __launch_bounds__(64 * WGM * WGN, OCC)
 dyad_gemm_mfma(GemmArgs a) {
     using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
@@ -205,6 +209,11 @@ dyad_gemm_mfma(GemmArgs a) {
     };
 
     // ---- registers (set `set`) -> LDS stage buffer
+    // the input operand as staged: GELU(in) with GELU_IN, else in itself
+    auto act = [](uint4 v) -> uint4 {
+        if constexpr (GELU_IN) return gelu8(v);
+        else return v;
+    };
     auto stash = [&](auto comp, uint16_t *buf, auto set) {
         constexpr bool C2 = decltype(comp)::value;
         auto &ra = ras[decltype(set)::value];
@@ -214,19 +223,23 @@ dyad_gemm_mfma(GemmArgs a) {
         for (int q = 0; q < C::kRC; ++q) {
             const int rc = tid + q * T, row = rc >> 2, c = rc & 3;
             if constexpr (!C2 || !(IN_T || OUT_T)) {
-                *reinterpret_cast<uint4 *>(buf + lds_off(row, c)) = ra[q][0];
+                *reinterpret_cast<uint4 *>(buf + lds_off(row, c)) = act(ra[q][0]);
             } else if constexpr (IN_T) {
                 uint4 span[D];
+                if constexpr (OUT_T) {
+                    // every residue of the span is used: activate it whole
 #pragma unroll
-                for (int d = 0; d < D; ++d) span[d] = ra[q][d];
-                if constexpr (OUT_T)
+                    for (int d = 0; d < D; ++d) span[d] = act(ra[q][d]);
                     deinterleave_all<D>(span, buf + lds_off(row, c), C::kSlab);
-                else   // only residue g1 feeds this tile
-                    *reinterpret_cast<uint4 *>(buf + lds_off(row, c)) = deinterleave_uniform<D>(span, g1);
+                } else {   // only residue g1 feeds this tile: activate its 8 values
+#pragma unroll
+                    for (int d = 0; d < D; ++d) span[d] = ra[q][d];
+                    *reinterpret_cast<uint4 *>(buf + lds_off(row, c)) = act(deinterleave_uniform<D>(span, g1));
+                }
             } else {
 #pragma unroll
                 for (int r = 0; r < D; ++r)
-                    *reinterpret_cast<uint4 *>(buf + r * C::kSlab + lds_off(row, c)) = ra[q][r];
+                    *reinterpret_cast<uint4 *>(buf + r * C::kSlab + lds_off(row, c)) = act(ra[q][r]);
             }
         }
         if constexpr (!W_T) {

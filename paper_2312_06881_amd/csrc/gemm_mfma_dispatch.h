@@ -53,7 +53,7 @@ inline bool gemm_split_ws(const GemmPass &p, int splits, hipStream_t s, GemmArgs
     return true;
 }
 
-template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int PF = 1>
+template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int PF = 1, bool GELU_IN = false>
 hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
     GemmArgs a;
@@ -78,7 +78,7 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     a.tiles_n = (int)tiles_n;
     a.tiles_total = (int)(tiles_m * tiles_n);
     gemm_split_ws(p, gemm_splits(p, a.tiles_total, PF), s, a);
-    dyad_gemm_mfma<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, occupancy<C>(), PF>
+    dyad_gemm_mfma<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, occupancy<C>(), PF, GELU_IN>
         <<<a.tiles_total * a.splits, C::kThreads, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && a.part) e = launch_split_reduce(p, a.part, a.splits, s);
@@ -395,6 +395,50 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     return hipErrorNotSupported;
 }
 
+// Forward of a layer whose input is GELU(in) (GemmPass::gelu_in): the phased
+// tiles, with the activation applied to the input operand as it is staged.
+// Tiles as for the plain forward pass (8-wave 256 x 192 / 256 x 256 where the
+// batch fills the GPU, else 4-wave tiles with split reductions), one stage of
+// loads ahead.  An output transpose at n_dyad 8 / 16 has no such tile.
+template <int D, bool IN_T, bool OUT_T>
+hipError_t dispatch_gelu_in(const GemmPass &p, hipStream_t s) {
+    if constexpr (OUT_T && D > 4) {
+        return hipErrorNotSupported;
+    } else {
+        if (p.bk % kStageK != 0) return hipErrorNotSupported;
+        auto enough = [&](int bm, int bn_tile) { return ((p.M + bm - 1) / bm) * (p.Nout / bn_tile) >= 256; };
+        if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
+            if (p.bn % 192 == 0 && enough(256, 192))
+                return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
+        if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+            if (p.bn % 256 == 0 && enough(256, 256))
+                return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, false, 1, true>(p, s);
+        constexpr int BM = D >= 8 ? 64 : 128;
+        constexpr int BM256 = OUT_T ? 64 : BM;
+        if constexpr (!OUT_T || (256 / D >= 16 && D < 16))
+            if (p.bn % 256 == 0) return launch_tile<BM256, 256, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
+        if constexpr (!OUT_T || (192 % D == 0 && (192 / D) % 16 == 0))
+            if (p.bn % 192 == 0) return launch_tile<BM, 192, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
+        if constexpr (!OUT_T || 128 / D >= 16)
+            if (p.bn % 128 == 0) return launch_tile<BM, 128, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
+        if constexpr (!OUT_T || 64 / D >= 16)
+            if (p.bn % 64 == 0) return launch_tile<BM, 64, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
+        return hipErrorNotSupported;
+    }
+}
+
+template <bool IN_T, bool OUT_T>
+hipError_t dispatch_d_gelu_in(const GemmPass &p, hipStream_t s) {
+    switch (p.D) {
+    case 1: return dispatch_gelu_in<1, IN_T, OUT_T>(p, s);
+    case 2: return dispatch_gelu_in<2, IN_T, OUT_T>(p, s);
+    case 4: return dispatch_gelu_in<4, IN_T, OUT_T>(p, s);
+    case 8: return dispatch_gelu_in<8, IN_T, OUT_T>(p, s);
+    case 16: return dispatch_gelu_in<16, IN_T, OUT_T>(p, s);
+    default: return hipErrorNotSupported;
+    }
+}
+
 template <bool IN_T, bool OUT_T, bool W_T>
 hipError_t dispatch_d(const GemmPass &p, hipStream_t s) {
     switch (p.D) {
@@ -414,5 +458,8 @@ hipError_t launch_mfma_fwd_dt(const GemmPass &p, hipStream_t s);
 hipError_t launch_mfma_dx_it(const GemmPass &p, hipStream_t s);
 hipError_t launch_mfma_dx_ot(const GemmPass &p, hipStream_t s);
 hipError_t launch_mfma_dx_dt(const GemmPass &p, hipStream_t s);
+hipError_t launch_mfma_fwd_gin_it(const GemmPass &p, hipStream_t s);
+hipError_t launch_mfma_fwd_gin_ot(const GemmPass &p, hipStream_t s);
+hipError_t launch_mfma_fwd_gin_dt(const GemmPass &p, hipStream_t s);
 
 }  // namespace dyad

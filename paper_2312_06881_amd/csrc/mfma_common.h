@@ -159,6 +159,16 @@ __device__ __forceinline__ float gelu_grad(float x) {
     return fmaf(x * e, 0.3989422804014327f, cdf);
 }
 
+// GELU of 8 packed bf16 values, each computed in fp32 and rounded once to
+// bf16 (RNE): the activated operand a layer after a GELU multiplies, formed as
+// the operand is staged.
+__device__ __forceinline__ uint4 gelu8(uint4 v) {
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) w[p] = pack_bf16(gelu(unpack_bf16(w[p], 0)), gelu(unpack_bf16(w[p], 1)));
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // 16 bytes to base + voff; dropped when voff lies past the buffer's range.
 __device__ __forceinline__ void bstore16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint4 v) {
     const u32x4_t w = {v.x, v.y, v.z, v.w};

@@ -4,10 +4,12 @@
   BlockTrans(W2) in the IT / OT / DT form (paper Sec. 2.2-2.4, Eqs. 1-16), a
   replacement for ``torch.nn.Linear``.
 * ``DyadFF``: the feed-forward block fc1 -> GELU -> fc2 with both layers Dyad,
-  each with its own variant if wanted (a heterogeneous mix, Sec. 4).  The
-  forward writes GELU(fc1) and stashes fc1's pre-activation in the same
-  epilogue; the backward applies GELU' inside fc2's input-gradient epilogue,
-  so the activation gradient is never a separate pass.
+  each with its own variant if wanted (a heterogeneous mix, Sec. 4).  Unfused,
+  the forward writes GELU(fc1) and stashes fc1's pre-activation in the same
+  epilogue; fused, fc1 writes only the pre-activation and fc2's forward and
+  weight-gradient kernels apply GELU as they stage it.  Either way the backward
+  applies GELU' inside fc2's input-gradient epilogue, so the activation
+  gradient is never a separate pass.
 
 Autograd runs every pass through the C-ABI (forward, input gradient, weight and
 bias gradient); there is no torch fallback and CPU tensors are rejected.
@@ -22,7 +24,7 @@ import math
 
 import torch
 
-from . import backward_dw, backward_dx, forward
+from . import DyadError, backward_dw, backward_dx, forward
 
 __all__ = ["DyadLinear", "DyadFF", "dyad_linear", "dyad_ff"]
 
@@ -52,29 +54,60 @@ class _DyadLinearFn(torch.autograd.Function):
         return dx, dw1, dw2, db, None, None
 
 
+_REFUSED = (-2, -4)   # DYAD_ERR_SHAPE, DYAD_ERR_DTYPE: no fused kernel for this layer
+
+
 class _DyadFFFn(torch.autograd.Function):
+    """fc1 -> GELU -> fc2.  Unfused: fc1's epilogue writes GELU(h) and stashes h.  Fused:
+    fc1 writes only its pre-activation h; fc2's forward and weight-gradient kernels apply
+    GELU to h as they stage it (dyad_forward_ex / dyad_backward_dw_ex), so GELU(h) is never
+    written.  Both: fc2's input-gradient epilogue multiplies by GELU'(h).  A layer the fused
+    kernels refuse runs unfused."""
+
     @staticmethod
-    def forward(ctx, x, w1a, w2a, ba, w1b, w2b, bb, variants, ffn, d_out):
+    def forward(ctx, x, w1a, w2a, ba, w1b, w2b, bb, variants, ffn, d_out, fused):
         va, vb = variants
-        a, h = forward(x, w1a, w2a, ba, va, act="gelu", stash_h=True, n_out=ffn)
-        y = forward(a, w1b, w2b, bb, vb, n_out=d_out)
+        y = None
+        if fused:
+            h = forward(x, w1a, w2a, ba, va, n_out=ffn)
+            try:
+                y = forward(h, w1b, w2b, bb, vb, n_out=d_out, act_in="gelu")
+                a = None
+            except DyadError as e:
+                if e.status not in _REFUSED:
+                    raise
+        if y is None:
+            a, h = forward(x, w1a, w2a, ba, va, act="gelu", stash_h=True, n_out=ffn)
+            y = forward(a, w1b, w2b, bb, vb, n_out=d_out)
         ctx.variants = variants
         ctx.bias = (ba is not None, bb is not None)
-        ctx.save_for_backward(x, h, a, w1a, w2a, w1b, w2b)
+        ctx.fused = a is None
+        ctx.save_for_backward(x, h, a, w1a, w2a, ba, w1b, w2b)
         return y
 
     @staticmethod
     def backward(ctx, dy):
-        x, h, a, w1a, w2a, w1b, w2b = ctx.saved_tensors
+        x, h, a, w1a, w2a, ba, w1b, w2b = ctx.saved_tensors
         va, vb = ctx.variants
         dy = dy.contiguous()
         # fc2: input gradient times GELU'(fc1 pre-activation), then its weights
         dz1 = backward_dx(dy, w1b, w2b, vb, act_in="gelu", h_in=h)
-        dw1b, dw2b, dbb = backward_dw(dy, a, w1b.shape[0], vb, want_db=ctx.bias[1])
+        dwb = None
+        if ctx.fused:
+            try:
+                dwb = backward_dw(dy, h, w1b.shape[0], vb, want_db=ctx.bias[1], act_in="gelu")
+            except DyadError as e:
+                if e.status not in _REFUSED:
+                    raise
+                # this weight gradient has no fused kernel: recompute GELU(h) through fc1
+                a, _ = forward(x, w1a, w2a, ba, va, act="gelu", stash_h=True, n_out=h.shape[1])
+        if dwb is None:
+            dwb = backward_dw(dy, a, w1b.shape[0], vb, want_db=ctx.bias[1])
+        dw1b, dw2b, dbb = dwb
         # fc1
         dx = backward_dx(dz1, w1a, w2a, va, n_in=x.shape[1]) if ctx.needs_input_grad[0] else None
         dw1a, dw2a, dba = backward_dw(dz1, x, w1a.shape[0], va, want_db=ctx.bias[0])
-        return dx, dw1a, dw2a, dba, dw1b, dw2b, dbb, None, None, None
+        return dx, dw1a, dw2a, dba, dw1b, dw2b, dbb, None, None, None, None
 
 
 def _variant_pair(variant):
@@ -94,14 +127,15 @@ def dyad_linear(x, w1, w2, bias=None, variant="IT", out_features=None):
     return y.reshape(*x.shape[:-1], out_features)
 
 
-def dyad_ff(x, fc1, fc2, variant="IT", ffn=None):
+def dyad_ff(x, fc1, fc2, variant="IT", ffn=None, fused=False):
     """Functional form of ``DyadFF``; fc1 / fc2 are (W1, W2, bias) triples; variant is one
     variant or an (fc1, fc2) pair; ffn is the hidden width (default n_dyad * fc1's bo).
-    The output width is x's, as the block is d -> ffn -> d."""
+    The output width is x's, as the block is d -> ffn -> d.  fused: GELU applied inside
+    fc2's kernels, the activation never written (see _DyadFFFn)."""
     d = x.shape[-1]
     if ffn is None:
         ffn = fc1[0].shape[0] * fc1[0].shape[1]
-    y = _DyadFFFn.apply(_tokens(x), *fc1, *fc2, _variant_pair(variant), ffn, d)
+    y = _DyadFFFn.apply(_tokens(x), *fc1, *fc2, _variant_pair(variant), ffn, d, bool(fused))
     return y.reshape(*x.shape[:-1], d)
 
 
@@ -149,10 +183,13 @@ class DyadFF(torch.nn.Module):
     """Feed-forward block fc1 (d -> ffn) -> GELU -> fc2 (ffn -> d), both Dyad layers.
 
     ``variant`` is one of IT / OT / DT for both layers, or an (fc1, fc2) pair for a
-    heterogeneous mix; ``n_dyad`` likewise may be one value or a pair."""
+    heterogeneous mix; ``n_dyad`` likewise may be one value or a pair.  ``fused``: fc1
+    writes only its pre-activation and fc2's kernels apply GELU as they stage it."""
 
-    def __init__(self, d, ffn, n_dyad, variant="IT", bias=True, device=None, dtype=torch.bfloat16):
+    def __init__(self, d, ffn, n_dyad, variant="IT", bias=True, device=None, dtype=torch.bfloat16,
+                 fused=False):
         super().__init__()
+        self.fused = fused
         va, vb = _variant_pair(variant)
         da, db = (n_dyad, n_dyad) if isinstance(n_dyad, int) else tuple(n_dyad)
         self.fc1 = DyadLinear(d, ffn, da, va, bias, device, dtype)
@@ -162,4 +199,4 @@ class DyadFF(torch.nn.Module):
 
     def forward(self, x):
         return dyad_ff(x, (self.fc1.w1, self.fc1.w2, self.fc1.bias),
-                       (self.fc2.w1, self.fc2.w2, self.fc2.bias), self.variant, self.ffn)
+                       (self.fc2.w1, self.fc2.w2, self.fc2.bias), self.variant, self.ffn, self.fused)

@@ -163,3 +163,24 @@ def test_dw_workspace_small_batch_has_no_copies():
     for v in ("IT", "OT", "DT"):
         b = dy.dyad_dw_workspace_bytes(dy.VARIANTS[v], 1024, 4096, 16, 512, dy.BF16)
         assert b % split_bytes == 0    # whole splits of partial sums, nothing else
+
+
+def test_ex_calls_reject_before_any_launch():
+    """The input-activation calls check their arguments like the plain ones, plus act_in
+    (a valid enum, bf16 only); these return before any HIP call."""
+    a = dict(variant=0, n_in=64, n_out=256, n_dyad=4, M=8, dtype=1, act_in=1, X=FAKE, W1=FAKE, W2=FAKE,
+             bias=None, act=0, Y=FAKE, H=None, stream=None)
+    assert dy.dyad_forward_ex(**{**a, "act_in": 7}) == -1
+    assert dy.dyad_forward_ex(**{**a, "dtype": 0}) == -4       # fp32 has no fused kernel
+    assert dy.dyad_forward_ex(**{**a, "variant": 5}) == -1
+    assert dy.dyad_forward_ex(**{**a, "X": FAKE + 2}) == -3
+    b = dict(variant=0, n_in=64, n_out=256, n_dyad=4, M=8, dtype=1, act_in=1, dZ=FAKE, X=FAKE, dW1=FAKE,
+             dW2=FAKE, dbias=None, workspace=None, workspace_bytes=0, stream=None)
+    assert dy.dyad_backward_dw_ex(**{**b, "act_in": 3}) == -1
+    assert dy.dyad_backward_dw_ex(**{**b, "dtype": 0}) == -4
+    assert dy.dyad_backward_dw_ex(**{**b, "dW1": None}) == -1
+    assert dy.dyad_dw_workspace_bytes_ex(0, 64, 256, 4, 8, 0, 1) == 0    # fp32: unsupported
+    # act_in NONE: the plain query
+    for v in (0, 1, 2):
+        assert (dy.dyad_dw_workspace_bytes_ex(v, 768, 3072, 4, 16384, 1, 0) ==
+                dy.dyad_dw_workspace_bytes(v, 768, 3072, 4, 16384, 1))

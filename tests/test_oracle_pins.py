@@ -344,6 +344,16 @@ def test_gelu_against_normal_cdf():
     assert math.isclose(oracle.gelu_grad(30.0), 1.0)
 
 
+def test_gelu_array_against_normal_cdf():
+    """The elementwise form used for a layer whose input is GELU(H): scipy's normal CDF,
+    any shape, and the scalar form bit for bit."""
+    x = np.random.default_rng(3).standard_normal((37, 11)) * 4.0
+    g = oracle.gelu_array(x)
+    assert g.shape == x.shape
+    np.testing.assert_allclose(g, x * scipy.stats.norm.cdf(x), rtol=1e-13, atol=1e-300)
+    assert all(g.flat[i] == oracle.gelu(x.flat[i]) for i in range(0, x.size, 7))
+
+
 # ---- widths that n_dyad does not divide: zero-padding (appendix, caveat on rectangular W) ----
 
 PADDED = [  # (n_in, n_out, D) with D dividing at most one width
