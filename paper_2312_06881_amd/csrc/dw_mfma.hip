@@ -4,7 +4,9 @@
 
 namespace dyad {
 
-// Adds the splits in order 0..S-1 and writes dW1, dW2 (and db) in bf16.
+// Adds the splits in order 0..S-1 and writes dW1, dW2 (and db) in bf16.  The
+// partial sums are read once and the results written once: both streamed
+// (non-temporal).
 __global__ void __launch_bounds__(256) dyad_dw_reduce(const float *part, const float *part_db, int splits,
                                                       int64_t per_comp, int64_t n_out, uint16_t *dW1,
                                                       uint16_t *dW2, uint16_t *db) {
@@ -16,16 +18,12 @@ __global__ void __launch_bounds__(256) dyad_dw_reduce(const float *part, const f
         const int64_t idx = is_db ? (e - n4) * 4 : e * 4;
         const float *src = is_db ? part_db + idx : part + idx;
         const int64_t stride = is_db ? n_out : 2 * per_comp;
-        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int q = 0; q < splits; ++q) {
-            const float4 v = *reinterpret_cast<const float4 *>(src + q * stride);
-            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-        }
-        uint2 o;
-        o.x = pack_bf16(s.x, s.y);
-        o.y = pack_bf16(s.z, s.w);
+        f32x4_t s = {0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < splits; ++q) s += __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(src + q * stride));
+        typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+        const u32x2_t o = {pack_bf16(s[0], s[1]), pack_bf16(s[2], s[3])};
         uint16_t *out = is_db ? db + idx : (idx < per_comp ? dW1 + idx : dW2 + (idx - per_comp));
-        *reinterpret_cast<uint2 *>(out) = o;
+        __builtin_nontemporal_store(o, reinterpret_cast<u32x2_t *>(out));
     }
 }
 

@@ -83,7 +83,7 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
         ADD ? buffer_rsrc(a.part + ((int64_t)a.slice0 * a.M + m0) * a.Nout, 2u * o_bytes) : rO;
     if (grad) {
 #pragma unroll
-        for (int q = 0; q < kQ; ++q) hq[0][q] = bload16(rH, voE[q], 0);
+        for (int q = 0; q < kQ; ++q) hq[0][q] = bload16_stream(rH, voE[q], 0);
     }
 
 #pragma unroll
@@ -125,7 +125,7 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
         __syncthreads();
         if (grad && i + 1 < C::kSubM) {
 #pragma unroll
-            for (int q = 0; q < kQ; ++q) hq[(i + 1) & 1][q] = bload16(rH, voE[q] + (uint32_t)(i + 1) * row16, 0);
+            for (int q = 0; q < kQ; ++q) hq[(i + 1) & 1][q] = bload16_stream(rH, voE[q] + (uint32_t)(i + 1) * row16, 0);
         }
 #pragma unroll
         for (int q = 0; q < kQ; ++q) {
