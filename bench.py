@@ -51,6 +51,10 @@ def parse():
                          "pre-activation; dyad_forward_ex / dyad_backward_dw_ex)")
     ap.add_argument("--sets", type=int, default=0,
                     help="buffer sets to rotate (default: enough that a set recurs after ~512 MiB of traffic)")
+    ap.add_argument("--summarize-counters", metavar="ROOT",
+                    help="turn rocprofv3 --pmc runs of --only CALL (subdirectories <call>_sq, <call>_fetch, "
+                         "<call>_write of ROOT, call written with ':' and '.' as '_') into "
+                         "profiles/counters_<workload>.txt")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("CALL", "FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs of --only CALL (FETCH_SIZE, WRITE_SIZE) into "
                          "profiles/traffic_<workload>.json")
@@ -236,6 +240,9 @@ def main():
     args = parse()
     if args.summarize_pmc:
         summarize_pmc(args, *args.summarize_pmc)
+        return
+    if args.summarize_counters:
+        summarize_counters(args, args.summarize_counters)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "libdyad runs on one GPU; --gpus must be 1 "
@@ -532,6 +539,82 @@ def summarize_pmc(args, call, fetch_dir, write_dir):
     with open(path, "w") as fh:
         json.dump(rec, fh, indent=1, sort_keys=True)
     print(json.dumps({call: rec["calls"][call]}))
+
+
+SQ_COUNTERS = ("SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES "
+               "SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE")
+N_SIMD, N_XCD = 1024, 8   # MI355X: 256 CUs x 4 SIMDs, in 8 XCDs
+
+
+def _launch_sums(rows, counters):
+    """Per launch of the call (its kernels between two copies): counter sums, and the copy's values."""
+    rows = sorted(rows, key=lambda r: int(r["Dispatch_Id"]))
+    copies = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+    big = max(int(r["Grid_Size"]) for r in copies) if copies else 0
+    launches, cur, kernels = [], {}, set()
+    for r in rows:
+        if "copyBuffer" in r["Kernel_Name"]:
+            if int(r["Grid_Size"]) == big and cur:
+                launches.append(cur)
+                cur = {}
+            continue
+        if r["Counter_Name"] in counters:
+            cur[r["Counter_Name"]] = cur.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            kernels.add(r["Kernel_Name"].split("(")[0])
+    if cur:
+        launches.append(cur)
+    copy = {}
+    for r in copies:
+        if int(r["Grid_Size"]) == big:
+            copy.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return launches, {k: sum(v) / len(v) for k, v in copy.items()}, sorted(kernels)
+
+
+def summarize_counters(args, root):
+    """One row per call: MFMA utilisation (SQ_VALU_MFMA_BUSY_CYCLES over N_SIMD x the GPU's active
+    cycles per XCD), waves' share of cycles waiting (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES), achieved
+    TFLOP/s from the counted MFMA work (512 FLOP per MOPS unit), and HBM bytes per launch
+    (FETCH_SIZE / WRITE_SIZE scaled by the same counters of a plain copy of known size)."""
+    import glob
+    lines = []
+    for sq_dir in sorted(glob.glob(os.path.join(root, "*_sq"))):
+        tag = os.path.basename(sq_dir)[:-3]
+        call = tag.replace("_fc", ":fc").replace("_fwd", ".fwd").replace("_dx", ".dx").replace("_dw", ".dw")
+        sq, _, kernels = _launch_sums(_pmc_rows(sq_dir), SQ_COUNTERS.split())
+        avg = {k: sum(l.get(k, 0.0) for l in sq) / len(sq) for k in SQ_COUNTERS.split()}
+        cycles = avg["GRBM_GUI_ACTIVE"] / N_XCD
+        mfma = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (N_SIMD * cycles) if cycles else 0.0
+        wait = avg["SQ_WAIT_INST_ANY"] / avg["SQ_WAVE_CYCLES"] if avg["SQ_WAVE_CYCLES"] else 0.0
+        flop = avg["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512
+        fb = wb = None
+        fdir, wdir = os.path.join(root, tag + "_fetch"), os.path.join(root, tag + "_write")
+        if os.path.isdir(fdir) and os.path.isdir(wdir):
+            fl, fc, _ = _launch_sums(_pmc_rows(fdir), ["FETCH_SIZE"])
+            wl, wc, _ = _launch_sums(_pmc_rows(wdir), ["WRITE_SIZE"])
+            fb = sum(l["FETCH_SIZE"] for l in fl) / len(fl) * 1024 * COPY_BYTES / (fc["FETCH_SIZE"] * 1024)
+            wb = sum(l["WRITE_SIZE"] for l in wl) / len(wl) * 1024 * COPY_BYTES / (wc["WRITE_SIZE"] * 1024)
+        lines.append((call, len(sq), cycles, mfma, wait, flop, fb, wb, kernels))
+    path = os.path.join(ROOT, "profiles", f"counters_{args.workload}.txt")
+    with open(path, "w") as fh:
+        fh.write(f"# Hardware counters per launch, workload {args.workload} (one MI355X, bf16), "
+                 f"kernel sources {kernel_source_hash()}.\n"
+                 f"# commands, per call C (tag T = C with ':' and '.' as '_'), each its own run:\n"
+                 f"#   rocprofv3 --pmc {SQ_COUNTERS} --output-format csv -d <root>/T_sq -o run -- "
+                 f"python -u bench.py --workload {args.workload} --only C --steps 5\n"
+                 f"#   rocprofv3 --pmc FETCH_SIZE ... -d <root>/T_fetch ...;  rocprofv3 --pmc WRITE_SIZE ... "
+                 f"-d <root>/T_write ...\n"
+                 f"#   python bench.py --workload {args.workload} --summarize-counters <root>\n"
+                 f"# mfma_util = SQ_VALU_MFMA_BUSY_CYCLES / ({N_SIMD} SIMDs x GRBM_GUI_ACTIVE / {N_XCD} XCDs);"
+                 f" wait = SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES;\n"
+                 f"# mfma_flop = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512; HBM bytes = FETCH_SIZE / WRITE_SIZE scaled by "
+                 f"what they read for a plain {COPY_BYTES >> 20} MiB copy in the same run.\n"
+                 f"{'call':12s} {'launches':>8s} {'cycles/XCD':>11s} {'mfma_util':>9s} {'wait':>6s} "
+                 f"{'mfma_GFLOP':>10s} {'fetch_MB':>9s} {'write_MB':>9s}  kernels\n")
+        for call, n, cyc, mf, wt, fl, fb, wb, ks in lines:
+            fh.write(f"{call:12s} {n:8d} {cyc:11.0f} {mf:9.3f} {wt:6.3f} {fl / 1e9:10.2f} "
+                     f"{'-' if fb is None else f'{fb / 1e6:9.1f}':>9s} {'-' if wb is None else f'{wb / 1e6:9.1f}':>9s}  "
+                     f"{'; '.join(k.replace('void dyad::', '') for k in ks)}\n")
+    print(open(path).read())
 
 
 def kernel_source_hash():
