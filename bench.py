@@ -271,12 +271,12 @@ def main():
         (_, i1, o1), = wl.layers
         i2, o2 = o1, i1
     # Buffer sets, rotated call by call: consecutive calls never touch the same
-    # buffers, and a set comes round again only after about 512 MiB of other
-    # calls' traffic (twice the 256 MB last-level cache), so small-batch calls
-    # read their weights from HBM, not from the cache.
+    # buffers, and a set comes round again only after about 1 GiB of other
+    # calls' traffic (four times the 256 MB last-level cache), so small-batch
+    # calls read their weights from HBM, not from the cache.
     mean_call = sum(algorithmic_bytes(k, n_in, n_out, D, M) for (_, n_in, n_out) in
                     ((None, i1, o1), (None, i2, o2)) for k in ("fwd", "dx", "dw")) / 6
-    n_sets = max(1, min(16, -(-(512 << 20) // int(mean_call))))
+    n_sets = max(1, min(16, -(-(1 << 30) // int(mean_call))))
     if args.sets:
         n_sets = args.sets
     layers = [(Layer(torch, i1, o1, D, M, 0, dev), Layer(torch, i2, o2, D, M, 1, dev)) for _ in range(n_sets)]

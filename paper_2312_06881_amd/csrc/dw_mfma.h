@@ -97,6 +97,7 @@ template <int D, int BJ, int BK, int WJN, int WKN>
 constexpr int mg_gb() {
     int best = 0, cost = 1 << 30;
     for (int gb = 1; gb <= D; gb *= 2) {
+        if (D % gb != 0) break;
         const int ga = D / gb;
         if (WJN % ga || WKN % gb || BJ % (16 * ga) || BK % (16 * gb)) continue;
         const int bytes = 2 * kStageK * (dw_row(D, BJ / ga) + dw_row(D, BK / gb));
@@ -550,7 +551,11 @@ hipError_t launch_dw_variant(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     if (pl.BJ == J_ && pl.BK == K_ && pl.WJN == WJ_ && pl.WKN == WK_) switch (p.D) {        \
         case 1: return launch_dw_cfg<1, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
         case 2: return launch_dw_cfg<2, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
+        case 3: if constexpr (XG) return hipErrorNotSupported;                              \
+                else return launch_dw_cfg<3, J_, K_, WJ_, WK_, IN_T, OUT_T, false>(p, pl, s); \
         case 4: return launch_dw_cfg<4, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
+        case 6: if constexpr (XG) return hipErrorNotSupported;                              \
+                else return launch_dw_cfg<6, J_, K_, WJ_, WK_, IN_T, OUT_T, false>(p, pl, s); \
         case 8: return launch_dw_cfg<8, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);       \
         case 16: return launch_dw_cfg<16, J_, K_, WJ_, WK_, IN_T, OUT_T, XG>(p, pl, s);     \
         default: return hipErrorNotSupported;                                               \

@@ -39,7 +39,9 @@ constexpr Cand kCands[] = {
 bool choose(const DwPass &p, DwPlan &pl) {
     if (p.dtype != kBF16 || p.M <= 0) return false;
     if (p.n_in != p.D * p.bi || p.n_out != p.D * p.bo) return false;  // zero-padded widths
-    if (p.D != 1 && p.D != 2 && p.D != 4 && p.D != 8 && p.D != 16) return false;
+    // n_dyad 3 and 6 on the plain path only (no GELU-staging instances)
+    const bool pow2 = p.D == 1 || p.D == 2 || p.D == 4 || p.D == 8 || p.D == 16;
+    if (!pow2 && !((p.D == 3 || p.D == 6) && !p.gelu_x)) return false;
     // 32-bit buffer offsets within one stage (32 token rows of the wider operand)
     if ((int64_t)kStageK * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;
     // A strided BlockTrans operand wants a configuration with an all-groups
@@ -89,10 +91,14 @@ bool choose(const DwPass &p, DwPlan &pl) {
 // d = 1024, 3-4x on the wide layer 8192 -> 32768 at 32768 tokens) and from
 // 256 with blocks of at least 512 (1.8-3.5x on the wide layer at 256 and
 // 1024 tokens), and at n_dyad 8 from 8192 (at 2048 tokens it lost by up to 15%).
+// At n_dyad 3 and 6 no all-groups layout exists (the group grid needs a power
+// of two), so the fused tiles would gather a strided operand 2 bytes at a
+// time: there the copies go first from 2048 tokens.
 bool dw_permuted(const DwPass &p) {
-    if ((p.D != 8 && p.D != 16) || (!p.in_t && !p.out_t)) return false;
+    const bool odd = p.D == 3 || p.D == 6;
+    if ((p.D != 8 && p.D != 16 && !odd) || (!p.in_t && !p.out_t)) return false;
     const bool wide = p.D == 16 && p.M >= 256 && p.bi >= 512 && p.bo >= 512;
-    if (!wide && p.M < (p.D == 16 ? 2048 : 8192)) return false;
+    if (!wide && p.M < (p.D == 16 || odd ? 2048 : 8192)) return false;
     if ((p.out_t && p.bo % 32 != 0) || (p.in_t && p.bi % 32 != 0)) return false;
     const int64_t cap = (int64_t)1 << 31;
     return !(p.out_t && p.M * p.n_out * 2 > cap) && !(p.in_t && p.M * p.n_in * 2 > cap);

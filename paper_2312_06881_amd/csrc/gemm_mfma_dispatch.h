@@ -181,9 +181,20 @@ constexpr int gemm_lds(int BM, int BN, int WGM, int D, bool OUT_T) {
     return operands > epi ? operands : epi;
 }
 
-template <int BM, int BN, int WGM, int D, bool OUT_T>
+// Under an output transpose every 16-column MFMA block holds one residue:
+// BN splits into D residues of a multiple of 16 columns each.
+constexpr bool out_cols_ok(int BN, int D) { return BN % D == 0 && (BN / D) % 16 == 0; }
+
+// ... and each wave's columns hold whole residues or a part of one.
+constexpr bool wave_cols_ok(int BN, int WGN, int D) {
+    const int wn = BN / WGN, cpr = BN / D;
+    return wn % cpr == 0 || cpr % wn == 0;
+}
+
+template <int BM, int BN, int WGM, int WGN, int D, bool OUT_T>
 constexpr bool tile_ok() {
-    return (!OUT_T || (BN % D == 0 && (BN / D) % 16 == 0)) && gemm_lds(BM, BN, WGM, D, OUT_T) <= 160 * 1024;
+    return (!OUT_T || (out_cols_ok(BN, D) && wave_cols_ok(BN, WGN, D))) &&
+           gemm_lds(BM, BN, WGM, D, OUT_T) <= 160 * 1024;
 }
 
 // The two components apart, for blocks too narrow for a tile (n_dyad 8 / 16
@@ -271,9 +282,15 @@ hipError_t launch_permuted_as(const GemmPass &p, bool in_t, bool out_t, hipStrea
     return e;
 }
 
+// n_dyad 3 and 6 under an output transpose: with power-of-two blocks no
+// tile of whole residues (a multiple of 16 columns of each of the D) lies
+// within one block, so the components run apart on the de-interleaved form.
+template <int D>
+constexpr bool odd_residues() { return D == 3 || D == 6; }
+
 template <int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t launch_permuted(const GemmPass &p, hipStream_t s) {
-    if constexpr (D < 8 || 64 % D != 0 || (!IN_T && !OUT_T)) {
+    if constexpr ((D < 8 && !odd_residues<D>()) || (D >= 8 && 64 % D != 0) || (!IN_T && !OUT_T)) {
         return hipErrorNotSupported;
     } else {
         if (p.bk % kStageK != 0 || p.Nout % 8 != 0) return hipErrorNotSupported;
@@ -304,6 +321,7 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
             const hipError_t e = launch_permuted<D, IN_T, OUT_T, W_T>(p, s);
             if (e != hipErrorNotSupported) return e;
         }
+    if constexpr (odd_residues<D>() && OUT_T) return launch_permuted<D, IN_T, OUT_T, W_T>(p, s);
     if constexpr (D <= 4) {
         // the fused-stage kernel (natural-layout weights, transpose reads) wins
         // for the input gradient without an output transpose
@@ -322,19 +340,19 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
             // the forward pass keeps two stages of loads in flight when the
             // group is at least two stages deep (measured 3-8% faster at
             // OPT-125m fc2; the input gradient's transposed weights spill)
-            if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
+            if constexpr (tile_ok<256, 192, 4, 2, D, OUT_T>())
                 if (p.bn % 192 == 0 && enough(256, 192)) {
                     if constexpr (!W_T)
                         if (p.bk >= 2 * kStageK) return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, W_T, 2>(p, s);
                     return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
                 }
         } else if (p.epilogue == kEpiGeluGrad) {
-            if constexpr (tile_ok<128, 384, 2, D, OUT_T>())
+            if constexpr (tile_ok<128, 384, 2, 4, D, OUT_T>())
                 if (p.bn % 384 == 0 && enough(128, 384)) return launch_tile<128, 384, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
-            if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
+            if constexpr (tile_ok<256, 192, 4, 2, D, OUT_T>())
                 if (p.bn % 192 == 0 && enough(256, 192)) return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
         } else if constexpr (OUT_T && !W_T) {
-            if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+            if constexpr (tile_ok<256, 256, 2, 4, D, OUT_T>())
                 if (p.bn % 256 == 0 && enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
         }
     }
@@ -346,17 +364,17 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
                 if constexpr (tile2_ok<128, 256, 2, 4, D, IN_T, OUT_T, W_T>())
                     if (enough(128, 256)) return launch_tile2<128, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
             } else if constexpr (D == 8 && OUT_T) {
-                if constexpr (tile_ok<128, 256, 2, D, OUT_T>())
+                if constexpr (tile_ok<128, 256, 2, 4, D, OUT_T>())
                     if (enough(128, 256)) return launch_tile<128, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
             } else if constexpr (D == 8) {
-                if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+                if constexpr (tile_ok<256, 256, 2, 4, D, OUT_T>())
                     if (enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
             } else if (p.epilogue == kEpiBias) {
                 if constexpr (OUT_T) {
-                    if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+                    if constexpr (tile_ok<256, 256, 2, 4, D, OUT_T>())
                         if (enough(256, 256)) return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, W_T>(p, s);
                 } else {
-                    if constexpr (tile_ok<256, 256, 4, D, OUT_T>())
+                    if constexpr (tile_ok<256, 256, 4, 2, D, OUT_T>())
                         if (enough(256, 256)) return launch_tile<256, 256, 4, 2, D, IN_T, OUT_T, W_T>(p, s);
                 }
             }
@@ -381,13 +399,13 @@ hipError_t dispatch_tiles(const GemmPass &p, hipStream_t s) {
     // with an output transpose a 128 x 256 tile's D slabs need one workgroup per
     // CU; 64 x 256 keeps two, which measures faster
     constexpr int BM256 = OUT_T ? 64 : BM;
-    if constexpr (!OUT_T || (256 / D >= 16 && D < 16))
+    if constexpr (D < 16 && tile_ok<BM256, 256, 2, 2, D, OUT_T>())
         if (p.bn % 256 == 0) return launch_tile<BM256, 256, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
-    if constexpr (!OUT_T || (192 % D == 0 && (192 / D) % 16 == 0))
+    if constexpr (tile_ok<BM, 192, 2, 2, D, OUT_T>())
         if (p.bn % 192 == 0) return launch_tile<BM, 192, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
-    if constexpr (!OUT_T || 128 / D >= 16)
+    if constexpr (tile_ok<BM, 128, 2, 2, D, OUT_T>())
         if (p.bn % 128 == 0) return launch_tile<BM, 128, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
-    if constexpr (!OUT_T || 64 / D >= 16)
+    if constexpr (tile_ok<BM, 64, 2, 2, D, OUT_T>())
         if (p.bn % 64 == 0) return launch_tile<BM, 64, 2, 2, D, IN_T, OUT_T, W_T>(p, s);
     // An output transpose whose blocks are too narrow for any tile above
     // (n_dyad 16 with blocks of 64 or 128 columns): the components run apart.
@@ -407,21 +425,21 @@ hipError_t dispatch_gelu_in(const GemmPass &p, hipStream_t s) {
     } else {
         if (p.bk % kStageK != 0) return hipErrorNotSupported;
         auto enough = [&](int bm, int bn_tile) { return ((p.M + bm - 1) / bm) * (p.Nout / bn_tile) >= 256; };
-        if constexpr (tile_ok<256, 192, 4, D, OUT_T>())
+        if constexpr (tile_ok<256, 192, 4, 2, D, OUT_T>())
             if (p.bn % 192 == 0 && enough(256, 192))
                 return launch_tile<256, 192, 4, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
-        if constexpr (tile_ok<256, 256, 2, D, OUT_T>())
+        if constexpr (tile_ok<256, 256, 2, 4, D, OUT_T>())
             if (p.bn % 256 == 0 && enough(256, 256))
                 return launch_tile<256, 256, 2, 4, D, IN_T, OUT_T, false, 1, true>(p, s);
         constexpr int BM = D >= 8 ? 64 : 128;
         constexpr int BM256 = OUT_T ? 64 : BM;
-        if constexpr (!OUT_T || (256 / D >= 16 && D < 16))
+        if constexpr (D < 16 && tile_ok<BM256, 256, 2, 2, D, OUT_T>())
             if (p.bn % 256 == 0) return launch_tile<BM256, 256, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
-        if constexpr (!OUT_T || (192 % D == 0 && (192 / D) % 16 == 0))
+        if constexpr (tile_ok<BM, 192, 2, 2, D, OUT_T>())
             if (p.bn % 192 == 0) return launch_tile<BM, 192, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
-        if constexpr (!OUT_T || 128 / D >= 16)
+        if constexpr (tile_ok<BM, 128, 2, 2, D, OUT_T>())
             if (p.bn % 128 == 0) return launch_tile<BM, 128, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
-        if constexpr (!OUT_T || 64 / D >= 16)
+        if constexpr (tile_ok<BM, 64, 2, 2, D, OUT_T>())
             if (p.bn % 64 == 0) return launch_tile<BM, 64, 2, 2, D, IN_T, OUT_T, false, 1, true>(p, s);
         return hipErrorNotSupported;
     }
@@ -444,7 +462,9 @@ hipError_t dispatch_d(const GemmPass &p, hipStream_t s) {
     switch (p.D) {
     case 1: return dispatch_tiles<1, IN_T, OUT_T, W_T>(p, s);
     case 2: return dispatch_tiles<2, IN_T, OUT_T, W_T>(p, s);
+    case 3: return dispatch_tiles<3, IN_T, OUT_T, W_T>(p, s);
     case 4: return dispatch_tiles<4, IN_T, OUT_T, W_T>(p, s);
+    case 6: return dispatch_tiles<6, IN_T, OUT_T, W_T>(p, s);
     case 8: return dispatch_tiles<8, IN_T, OUT_T, W_T>(p, s);
     case 16: return dispatch_tiles<16, IN_T, OUT_T, W_T>(p, s);
     default: return hipErrorNotSupported;

@@ -72,17 +72,19 @@ __device__ __forceinline__ uint4 deinterleave(const uint4 (&v)[D]) {
 
 // Residue r (0 <= r < D, uniform across the workgroup, known only at run
 // time) of the span, without branches: element e = 2wD + r sits in vector
-// e / 8 (a compile-time base, plus one when r carries it over, which only
-// n_dyad 16 can do), word (e % 8) / 2 and half r % 2, so each output word is
+// e / 8 (a compile-time base, plus one when r carries it over, which happens
+// unless D divides 8), word (e % 8) / 2 and half e % 2, so each output word is
 // a select or two and one v_perm_b32.  Branch-free code keeps a pipelined main
 // loop straight-line, which the compiler needs to wait on exact load counts.
 template <int D>
 __device__ __forceinline__ uint32_t span_word(const uint4 (&v)[D], int c, int r) {
+    // at most one carry: (c % 8) + r < 16 for every n_dyad up to 9, and c % 8 == 0 at 16
+    static_assert(D <= 9 || D == 16, "one vector of carry");
     // element c + r, c a multiple of D fixed at compile time after unrolling;
-    // below n_dyad 16 the vector is c / 8 for every r < D
+    // when D divides 8 the vector is c / 8 for every r < D
     const int base = c >> 3;
     uint4 x = v[base];
-    if constexpr (D > 8)
+    if constexpr (8 % D != 0)
         if (((c & 7) + r) >= 8) x = v[base + 1 < D ? base + 1 : base];
     return word_of(x, ((c + r) & 7) >> 1);
 }
@@ -90,6 +92,7 @@ __device__ __forceinline__ uint32_t span_word(const uint4 (&v)[D], int c, int r)
 template <int D>
 __device__ __forceinline__ uint4 deinterleave_uniform(const uint4 (&v)[D], int r) {
     uint32_t o[4];
+    // elements 2wD + r and (2w + 1)D + r: halves r % 2 and (r + D) % 2
     const uint32_t sel = perm_sel((r & 1) * 2, 4 + ((r + D) & 1) * 2);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {

@@ -500,9 +500,10 @@ hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices,
 
 // out[n][g*bk + k] = in[n][k*D + g] for a token row of D*bk elements: the
 // input columns of residue g made the contiguous block g.  A group of 4*D
-// threads moves 32 reduction indices of one row (D divides 64): 16-byte loads
-// of the row span into LDS, then per thread 8 indices of one residue, stored
-// as 16 bytes.
+// threads moves 32 reduction indices of one row: 16-byte loads of the row
+// span into LDS, then per thread 8 indices of one residue, stored as 16
+// bytes.  A block holds 256 / (4*D) groups; where 4*D does not divide 256 its
+// last threads have no group and stay idle.
 __global__ void __launch_bounds__(256) deinterleave_kernel(const uint16_t *in, uint16_t *out, int64_t M, int bk,
                                                            int D) {
     __shared__ uint4 buf[256];
@@ -510,7 +511,7 @@ __global__ void __launch_bounds__(256) deinterleave_kernel(const uint16_t *in, u
     const int c = tid / per, pc = tid % per;
     const int spans = bk / 32;
     const int64_t gc = (int64_t)blockIdx.x * (256 / per) + c;
-    const bool ok = gc < M * spans;
+    const bool ok = c < 256 / per && gc < M * spans;
     const int64_t n = ok ? gc / spans : 0, kc = ok ? gc % spans : 0;
     const int64_t Kin = (int64_t)bk * D;
     if (ok) buf[tid] = *reinterpret_cast<const uint4 *>(in + n * Kin + kc * 32 * D + pc * 8);
@@ -526,7 +527,7 @@ __global__ void __launch_bounds__(256) deinterleave_kernel(const uint16_t *in, u
 }
 
 hipError_t launch_deinterleave(const uint16_t *in, uint16_t *out, int64_t M, int64_t bk, int D, hipStream_t s) {
-    if (D < 1 || 64 % D != 0 || bk % 32 != 0 || M < 0) return hipErrorNotSupported;
+    if (D < 1 || D > 64 || bk % 32 != 0 || M < 0) return hipErrorNotSupported;
     if (M == 0) return hipSuccess;
     const int64_t groups = M * (bk / 32), per_block = 256 / (4 * D);
     const int64_t blocks = (groups + per_block - 1) / per_block;

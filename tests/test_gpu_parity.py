@@ -247,7 +247,10 @@ PADDED = [  # (n_in, n_out, n_dyad, M)
     (5, 9, 8, 17),         # n_dyad above n_in: three groups see only padding
     (250, 510, 4, 1100),   # enough tokens to split the weight gradient (ragged last split)
     (768, 3072, 5, 600),
-    (768, 3072, 3, 700),   # n_dyad 3 divides both widths; general kernels all the same
+    (768, 3072, 3, 700),   # n_dyad 3 divides both widths, not the blocks (256, 1024)
+    (768, 3072, 6, 300),   # blocks of 128 and 512
+    (1536, 384, 6, 257),   # blocks of 256 and 64
+    (384, 1536, 3, 2100),  # enough tokens for the de-interleaved forms of every pass
 ]
 
 
@@ -343,10 +346,10 @@ def check_full_layer(n_in, n_out, D, M, variant, fwd_act="none", dx_act="none", 
     x, w1, w2, b, dz = (gpu(t) for t in (L.X, L.W1, L.W2, L.bias, L.dZ))
     h_in = gpu(L.H_in) if dx_act == "gelu" else None
     if fwd_act == "gelu":
-        y, h = dy.forward(x, w1, w2, b, variant=variant, act="gelu", stash_h=True)
+        y, h = dy.forward(x, w1, w2, b, variant=variant, act="gelu", stash_h=True, n_out=n_out)
     else:
-        y, h = dy.forward(x, w1, w2, b, variant=variant), None
-    dx = dy.backward_dx(dz, w1, w2, variant=variant, act_in=dx_act, h_in=h_in)
+        y, h = dy.forward(x, w1, w2, b, variant=variant, n_out=n_out), None
+    dx = dy.backward_dx(dz, w1, w2, variant=variant, act_in=dx_act, h_in=h_in, n_in=n_in)
     dw1, dw2, db = dy.backward_dw(dz, x, D, variant=variant)
     torch.cuda.synchronize()
     del x, dz, h_in
@@ -366,7 +369,7 @@ def check_full_layer(n_in, n_out, D, M, variant, fwd_act="none", dx_act="none", 
     del dx
     rng = np.random.default_rng(11)
     n = 300
-    bo, bi = n_out // D, n_in // D
+    bo, bi = -(-n_out // D), -(-n_in // D)   # zero-padded blocks where D does not divide
     comp = rng.integers(1, 3, n)
     i, j, k = rng.integers(0, D, n), rng.integers(0, bo, n), rng.integers(0, bi, n)
     comp[:4], i[:4], j[:4], k[:4] = [1, 2, 1, 2], [0, 0, D - 1, D - 1], [0, 0, bo - 1, bo - 1], [0, 0, bi - 1, bi - 1]
@@ -391,6 +394,18 @@ def test_full_size_ff_sampled(wl, variant):
         banner("full", wl.name, name, variant)
         fa, da = FF_ACTS[name]
         check_full_layer(n_in, n_out, wl.n_dyad, wl.M, variant, fa, da, seed_offset=li)
+
+
+# OPT-125m feed-forward widths at n_dyad 3 and 6 (blocks 256 / 1024 and 128 /
+# 512, which n_dyad does not divide: the forward pass under an output
+# transpose runs its components apart) and 5 (zero-padded blocks of 154 / 615).
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("D", [3, 5, 6])
+def test_full_size_odd_dyad_sampled(D, variant):
+    for li, (name, n_in, n_out) in enumerate(OPT125M.layers):
+        banner("full odd", D, name, variant)
+        fa, da = FF_ACTS[name]
+        check_full_layer(n_in, n_out, D, OPT125M.M, variant, fa, da, seed_offset=li)
 
 
 @pytest.mark.parametrize("variant", VARIANTS)
