@@ -57,6 +57,7 @@ struct DwArgs {
     int tiles_j, tiles_k; // BJ x BK tiles per (component, group)
     int splits, items;    // items = splits * 2 * D * tiles_j * tiles_k
     int want_db;
+    int groups;           // D (the kernels on block-ordered operands take it at run time)
 };
 
 constexpr int kDwLdsBudget = 160 * 1024;
@@ -368,7 +369,7 @@ __device__ __forceinline__ void dw_tile(const DwArgs &a, unsigned char *smem, in
     // one split: bf16 results straight to dW1 / dW2 / db; else fp32 partial
     // sums -> workspace [split][comp][g][j][k], added by dyad_dw_reduce
     const int gout = MG ? gw : g;
-    const int64_t per_comp = (int64_t)D * bo * bi;
+    const int64_t per_comp = (int64_t)a.groups * bo * bi;
     if (a.direct) {
         // each 16-row slice of the wave's block goes through the wave's own
         // LDS area (the stage buffers are free after the last barrier) and
@@ -440,7 +441,7 @@ dyad_dw_mfma(DwArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[K::kLds];
     // work item -> (split, component, tile), split-major
     const int item = xcd_tile(blockIdx.x, a.items);
-    const int tiles = D * a.tiles_j * a.tiles_k;          // items per component and split
+    const int tiles = a.groups * a.tiles_j * a.tiles_k;   // items per component and split
     const int split = item / (2 * tiles);
     const int t2 = item % (2 * tiles);
     const int comp = t2 / tiles, t = t2 % tiles;
@@ -485,7 +486,8 @@ hipError_t launch_dw_cfg(const DwPass &p, const DwPlan &pl, hipStream_t s) {
     a.tokens_per_split = pl.tokens_per_split;
     a.tiles_j = pl.tiles_j; a.tiles_k = pl.tiles_k;
     a.splits = pl.splits;
-    a.items = pl.splits * 2 * D * pl.tiles_j * pl.tiles_k;
+    a.groups = (int)p.D;
+    a.items = pl.splits * 2 * a.groups * pl.tiles_j * pl.tiles_k;
     a.want_db = p.db != nullptr;
     if (pl.tokens_per_split >= p.M && p.M <= kStageK)   // one split of one stage
         dyad_dw_mfma<D, BJ, BK, WJN, WKN, IN_T, OUT_T, true, XG><<<(unsigned)a.items, C::kThreads, 0, s>>>(a);
@@ -535,7 +537,7 @@ inline bool dw_mg_available(int D, int BJ, int BK, int WJN, int WKN) {
 }
 
 // Per-variant launchers (one translation unit each); launch_dw_plain: both
-// components on block-ordered operands (n_dyad 8 and 16).
+// components on block-ordered operands (any n_dyad).
 hipError_t launch_dw_plain(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_it(const DwPass &p, const DwPlan &pl, hipStream_t s);
 hipError_t launch_dw_ot(const DwPass &p, const DwPlan &pl, hipStream_t s);

@@ -39,9 +39,11 @@ constexpr Cand kCands[] = {
 bool choose(const DwPass &p, DwPlan &pl) {
     if (p.dtype != kBF16 || p.M <= 0) return false;
     if (p.n_in != p.D * p.bi || p.n_out != p.D * p.bo) return false;  // zero-padded widths
-    // n_dyad 3 and 6 on the plain path only (no GELU-staging instances)
+    // n_dyad 3 and 6 without GELU staging, and any n_dyad on block-ordered
+    // operands (no transpose: the kernel takes n_dyad at run time)
     const bool pow2 = p.D == 1 || p.D == 2 || p.D == 4 || p.D == 8 || p.D == 16;
-    if (!pow2 && !((p.D == 3 || p.D == 6) && !p.gelu_x)) return false;
+    const bool plain = !p.in_t && !p.out_t && !p.gelu_x;
+    if (!pow2 && !plain && !((p.D == 3 || p.D == 6) && !p.gelu_x)) return false;
     // 32-bit buffer offsets within one stage (32 token rows of the wider operand)
     if ((int64_t)kStageK * (p.n_in > p.n_out ? p.n_in : p.n_out) * 2 >= ((int64_t)1 << 31)) return false;
     // A strided BlockTrans operand wants a configuration with an all-groups
@@ -104,28 +106,56 @@ bool dw_permuted(const DwPass &p) {
     return !(p.out_t && p.M * p.n_out * 2 > cap) && !(p.in_t && p.M * p.n_in * 2 > cap);
 }
 
-// The plan a pass runs with (for the permuted form, that of plain operands).
-// With GELU(X) the fused form always runs: the activation is applied where X
-// is staged, which the block-ordered copies would bypass.
-bool plan(const DwPass &p, DwPlan &pl, bool *permuted) {
-    *permuted = false;
+// Zero-padded form, for shapes no fused tile takes (widths n_dyad does not
+// divide, blocks that are not whole tiles, an n_dyad without tiles):
+// block-ordered copies of dZ and X with blocks padded to a multiple of 64
+// (component 2's from the residues under a transpose), the plain tiles over
+// them into padded gradients, then the real ones.  q: the padded pass.
+bool dw_pad_pass(const DwPass &p, DwPass &q) {
+    if (p.dtype != kBF16 || p.gelu_x || p.M < kPadMinTokens) return false;
+    if (p.n_in % 8 != 0 || p.n_out % 8 != 0 || p.n_in > kPadMaxRow || p.n_out > kPadMaxRow) return false;
+    q = p;
+    q.bi = pad_up(p.bi, 64);
+    q.bo = pad_up(p.bo, 64);
+    q.n_in = p.D * q.bi;
+    q.n_out = p.D * q.bo;
+    q.in_t = q.out_t = false;
+    // each copy within 2 GiB (32-bit buffer offsets across a split's tokens)
+    const int64_t cap = (int64_t)1 << 31;
+    return p.M * q.n_out * 2 <= cap && p.M * q.n_in * 2 <= cap;
+}
+
+enum class DwForm { kFused, kPermuted, kPadded };
+
+// The plan a pass runs with (for the permuted and padded forms, that of their
+// block-ordered pass).  With GELU(X) the fused form always runs: the
+// activation is applied where X is staged, which the copies would bypass.
+bool plan(const DwPass &p, DwPlan &pl, DwForm *form, DwPass *padded = nullptr) {
+    *form = DwForm::kFused;
     if (!p.gelu_x && dw_permuted(p)) {
         DwPass q = p;
         q.in_t = q.out_t = false;
         if (choose(q, pl)) {
-            *permuted = true;
+            *form = DwForm::kPermuted;
             return true;
         }
     }
-    return choose(p, pl);
+    if (choose(p, pl)) return true;
+    DwPass q;
+    if (dw_pad_pass(p, q) && choose(q, pl)) {
+        *form = DwForm::kPadded;
+        if (padded) *padded = q;
+        return true;
+    }
+    return false;
 }
 
 }  // namespace
 
 bool mfma_dw_ok(const DwPass &p) {
     DwPlan pl;
-    bool permuted;
-    return plan(p, pl, &permuted);
+    DwForm form;
+    return plan(p, pl, &form);
 }
 
 // Partial-sum bytes of plan pl (one split writes the results directly).
@@ -141,23 +171,72 @@ static size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
 static size_t copy_bytes_z(const DwPass &p) { return p.out_t ? (size_t)p.M * (size_t)p.n_out * 2 : 0; }
 static size_t copy_bytes_x(const DwPass &p) { return p.in_t ? (size_t)p.M * (size_t)p.n_in * 2 : 0; }
 
+// The padded form's workspace after the partial sums: the copies of dZ
+// (component 1, then component 2 under an output transpose) and of X (the
+// same under an input transpose), then the padded dW1, dW2 and db.
+struct DwPadLayout {
+    size_t z1, z2, x1, x2, w1, w2, db, end;
+};
+static DwPadLayout pad_layout(const DwPass &p, const DwPass &q, const DwPlan &pl) {
+    DwPadLayout l;
+    const size_t zb = round256((size_t)p.M * (size_t)q.n_out * 2), xb = round256((size_t)p.M * (size_t)q.n_in * 2);
+    const size_t wb = round256((size_t)(q.D * q.bo * q.bi) * 2);
+    l.z1 = round256(plan_workspace(q, pl));
+    l.z2 = l.z1 + zb;
+    l.x1 = l.z2 + (p.out_t ? zb : 0);
+    l.x2 = l.x1 + xb;
+    l.w1 = l.x2 + (p.in_t ? xb : 0);
+    l.w2 = l.w1 + wb;
+    l.db = l.w2 + wb;
+    l.end = l.db + (size_t)q.n_out * 2;
+    return l;
+}
+
 // Workspace of the plan a pass runs with: the partial sums, then (permuted
-// form) the copies, each starting on a 256-byte boundary.  The library
-// allocates nothing for the weight gradient; all of it comes from the caller.
+// and padded forms) the copies, each starting on a 256-byte boundary.  The
+// library allocates nothing for the weight gradient; all of it comes from
+// the caller.
 size_t mfma_dw_workspace(const DwPass &p) {
     DwPlan pl;
-    bool permuted;
-    if (!plan(p, pl, &permuted)) return 0;
+    DwForm form;
+    DwPass q;
+    if (!plan(p, pl, &form, &q)) return 0;
+    if (form == DwForm::kPadded) return pad_layout(p, q, pl).end;
     size_t b = plan_workspace(p, pl);
-    if (permuted) b = round256(b) + round256(copy_bytes_z(p)) + copy_bytes_x(p);
+    if (form == DwForm::kPermuted) b = round256(b) + round256(copy_bytes_z(p)) + copy_bytes_x(p);
     return b;
 }
 
 hipError_t launch_mfma_dw(const DwPass &p, hipStream_t s) {
     DwPlan pl;
-    bool permuted;
-    if (!plan(p, pl, &permuted)) return hipErrorNotSupported;
-    if (permuted) {
+    DwForm form;
+    DwPass q;
+    if (!plan(p, pl, &form, &q)) return hipErrorNotSupported;
+    if (form == DwForm::kPadded) {
+        const DwPadLayout l = pad_layout(p, q, pl);
+        unsigned char *ws = static_cast<unsigned char *>(p.ws);
+        auto at = [&](size_t off) { return reinterpret_cast<uint16_t *>(ws + off); };
+        DwPass r = q;
+        r.dZ = at(l.z1);
+        r.dZ2 = p.out_t ? at(l.z2) : nullptr;
+        r.X = at(l.x1);
+        r.X2 = p.in_t ? at(l.x2) : nullptr;
+        r.dW1 = at(l.w1);
+        r.dW2 = at(l.w2);
+        r.db = p.db ? at(l.db) : nullptr;
+        hipError_t e = launch_pad_rows(static_cast<const uint16_t *>(p.dZ), p.M, p.n_out, (int)p.D, p.bo, q.bo,
+                                       at(l.z1), p.out_t ? at(l.z2) : nullptr, s);
+        if (e == hipSuccess)
+            e = launch_pad_rows(static_cast<const uint16_t *>(p.X), p.M, p.n_in, (int)p.D, p.bi, q.bi, at(l.x1),
+                                p.in_t ? at(l.x2) : nullptr, s);
+        if (e == hipSuccess) e = launch_dw_plain(r, pl, s);
+        if (e == hipSuccess)
+            e = launch_unpad_dw(at(l.w1), at(l.w2), at(l.db), p.D, p.bo, p.bi, q.bo, q.bi, p.n_out,
+                                static_cast<uint16_t *>(p.dW1), static_cast<uint16_t *>(p.dW2),
+                                static_cast<uint16_t *>(p.db), s);
+        return e;
+    }
+    if (form == DwForm::kPermuted) {
         // the caller's workspace holds mfma_dw_workspace(p) bytes (checked by
         // the C-ABI): partial sums first, then the copies
         DwPass q = p;

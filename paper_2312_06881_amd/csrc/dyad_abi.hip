@@ -50,6 +50,7 @@ int launch_status(hipError_t e) { return e == hipSuccess ? DYAD_OK : DYAD_ERR_LA
 int run_gemm(const GemmPass &p, hipStream_t s) {
     hipError_t e = dyad::skinny_ok(p) ? dyad::launch_skinny_gemm(p, s) : hipErrorNotSupported;
     if (e == hipErrorNotSupported) e = dyad::launch_mfma_gemm(p, s);
+    if (e == hipErrorNotSupported) e = dyad::launch_padded_gemm(p, s);
     if (e == hipErrorNotSupported) e = dyad::launch_general_mfma_gemm(p, s);
     if (e == hipErrorNotSupported) e = dyad::launch_simt_gemm(p, s);
     return launch_status(e);

@@ -135,6 +135,30 @@ inline bool permuted_pays(int D, bool out_t, bool w_t, int64_t M, int64_t bk) {
     return bk >= 512;
 }
 
+// Zero-padded forms (padded_mfma.h): block-ordered copies padded to whole
+// tiles, for shapes the fused tiles refuse, from kPadMinTokens tokens.
+constexpr int64_t kPadMinTokens = 512;     // below this the general kernels run
+constexpr int64_t kPadMaxRow = 16384;      // widest row the padding copy stages in LDS
+constexpr int64_t pad_up(int64_t v, int64_t q) { return (v + q - 1) / q * q; }
+// dst1[m][g*bp + k] = src[m][g*b + k] and dst2[m][g*bp + k] = src[m][k*D + g]
+// for k < b and a source column below W, else 0 (either output may be null).
+hipError_t launch_pad_rows(const uint16_t *src, int64_t M, int64_t W, int D, int64_t b, int64_t bp,
+                           uint16_t *dst1, uint16_t *dst2, hipStream_t s);
+// dst[g][r][c] = src[g][r][c] for r < R and c < C, else 0 (dst is D x Rp x Cp).
+hipError_t launch_pad_matrix(const uint16_t *src, int64_t D, int64_t R, int64_t C, int64_t Rp, int64_t Cp,
+                             uint16_t *dst, hipStream_t s);
+// dW1 / dW2 [D][bo][bi] and db [n_out] (nullable) from their padded forms
+// [D][bop][bip] and [D * bop].
+hipError_t launch_unpad_dw(const uint16_t *p1, const uint16_t *p2, const uint16_t *pdb, int64_t D, int64_t bo,
+                           int64_t bi, int64_t bop, int64_t bip, int64_t n_out, uint16_t *dW1, uint16_t *dW2,
+                           uint16_t *db, hipStream_t s);
+// Forward / input gradient on the padded forms; hipErrorNotSupported, launching
+// nothing, for fp32, an input activation, fewer than kPadMinTokens tokens, an
+// input width that is not a multiple of 8 or above kPadMaxRow, or no workspace.
+hipError_t launch_padded_gemm(const GemmPass &p, hipStream_t s);
+hipError_t launch_padded_fwd(const GemmPass &p, hipStream_t s);
+hipError_t launch_padded_dx(const GemmPass &p, hipStream_t s);
+
 // MFMA grouped GEMM (bf16): returns hipErrorNotSupported, launching nothing,
 // when the pass's shape has no matching tile configuration (zero-padded
 // widths included).

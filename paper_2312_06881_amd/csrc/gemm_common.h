@@ -2,6 +2,8 @@
 // epilogue (accumulators -> bias / GELU / GELU' -> bf16 output).
 #pragma once
 
+#include <type_traits>
+
 #include "dyad_internal.h"
 #include "mfma_common.h"
 
@@ -18,6 +20,10 @@ struct GemmArgs {
     int splits;         // workgroups along the reduction per tile
     int slice0;         // partial slice of split 0
     int unperm;         // partial sums of column j*D + g belong to column g*bn + j
+    // zero-padded forms (gemm_epilogue_pad): component 2's block-ordered input,
+    // and the real output width and block size (Nout and bn are the padded ones)
+    const uint16_t *in2;
+    int64_t Nout_r, bn_r;
 };
 
 // Epilogue of a BM x BN tile whose accumulators sit in the MFMA layout (wave w
@@ -188,6 +194,153 @@ __device__ __forceinline__ void gemm_epilogue_as(const GemmArgs &a, unsigned cha
             }
             bstore16(rO, vo, make_uint4(pack_bf16(x[0], x[1]), pack_bf16(x[2], x[3]), pack_bf16(x[4], x[5]),
                                         pack_bf16(x[6], x[7])));
+        }
+    }
+}
+
+// Epilogue of a tile over zero-padded block-ordered operands (the padded
+// forms of a pass whose widths or blocks fit no tile).  The tile's columns
+// lie in one padded block g of a.bn columns; column n0 + t is real column
+// cbase + t (cbase = g * a.bn_r + n0 % a.bn) while t < nt, the real columns
+// left in the block and the row; the rest is padding and is dropped.  Real
+// rows have a.Nout_r columns, and a real block need not start on a 16-byte
+// boundary, so the accumulators are staged in LDS shifted by cbase % 8:
+// 8-column units aligned in the real row are then aligned in LDS as well.
+// Whole units (all 8 columns real) move as 16 bytes; the at most two ragged
+// units of a row (the tile's ends) go element by element in a pass of their
+// own, so no wave carries both forms.  Bias, the stashed pre-activation, the
+// GELU' input and the output sit at real columns.  ADD: each sum first gets
+// the fp32 sum of component 2 from slice a.slice0 of a.part (padded block
+// order, rows of a.Nout) at column (c % D) * a.bn + c / D of real column c
+// (component 2 under an output transpose).
+template <class C, int BM, int BN, bool ADD>
+__device__ __forceinline__ void gemm_epilogue_pad(const GemmArgs &a, unsigned char *smem,
+                                                  const f32x4_t (&acc)[C::kSubM][C::kSubN], int64_t m0, int n0,
+                                                  int64_t rows_left, int tid, int lane, int wave, int wn0) {
+    constexpr int T = C::kThreads;
+    constexpr int kPitch = BN + 12;                // room for the shift, rows 16-byte aligned
+    constexpr int kElems = C::kEpiRows * kPitch;
+    static_assert(2 * kElems * 4 <= C::kLds, "two shifted staging buffers fit the tile's LDS");
+    const bool grad = a.epilogue == kEpiGeluGrad;
+    const bool act = a.epilogue == kEpiBiasGelu;
+    const bool bias = a.bias != nullptr && !grad;
+    const bool keep_h = act && a.h_out != nullptr;
+    const int D = (int)a.D, bnp = (int)a.bn, bnr = (int)a.bn_r;
+    const uint32_t Nr = (uint32_t)a.Nout_r, Np = (uint32_t)a.Nout;
+    const uint32_t rows_t = (uint32_t)(rows_left < BM ? rows_left : BM);
+    const __amdgpu_buffer_rsrc_t rO = buffer_rsrc(a.out + m0 * a.Nout_r, rows_t * Nr * 2u);
+    const uint16_t *hbase = grad ? a.h_in : a.h_out;
+    const __amdgpu_buffer_rsrc_t rH = buffer_rsrc((hbase ? hbase : a.out) + m0 * a.Nout_r, rows_t * Nr * 2u);
+    const __amdgpu_buffer_rsrc_t rS =
+        buffer_rsrc(ADD ? a.part + ((int64_t)a.slice0 * a.M + m0) * a.Nout : nullptr, ADD ? rows_t * Np * 4u : 0u);
+    const int g = n0 / bnp, j0 = n0 - g * bnp;
+    const int cbase = g * bnr + j0;
+    int nt = bnr - j0 < BN ? bnr - j0 : BN;
+    if ((int)Nr - cbase < nt) nt = (int)Nr - cbase;
+    const int sh = cbase & 7, ubase = cbase - sh;
+    // units (8 LDS columns 8u .. 8u + 7 = real columns ubase + 8u ..): whole
+    // ones u_lo .. u_hi - 1, ragged ones 0 (when shifted) and u_hi (when a tail is left)
+    const bool vec = Nr % 8 == 0;
+    const int u_lo = vec ? (sh ? 1 : 0) : 0, u_hi = vec && nt > 0 ? (nt + sh) / 8 : 0;
+    const int n_whole = u_hi > u_lo ? u_hi - u_lo : 0;
+    // a tail unit u_hi unless unit 0 already holds the tail (nt + sh < 8)
+    const bool tail = (nt + sh) % 8 != 0 && !(sh && u_hi == 0);
+    int n_rag = vec ? (sh ? 1 : 0) + (tail ? 1 : 0) : (nt + sh + 7) / 8;
+    if (nt <= 0) n_rag = 0;
+
+    // the epilogue of one unit; WHOLE: all 8 columns real (and 16-byte aligned)
+    auto unit = [&](auto whole_tag, const float *ldsE, int erow, int u, int i) __attribute__((always_inline)) {
+        constexpr bool WHOLE = decltype(whole_tag)::value;
+        const int t0 = 8 * u - sh, r0 = ubase + 8 * u;
+        const float *src = ldsE + erow * kPitch + 8 * u;
+        const float4 lo = *reinterpret_cast<const float4 *>(src);
+        const float4 hi = *reinterpret_cast<const float4 *>(src + 4);
+        float x[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const uint32_t row = (uint32_t)((erow / 16) * C::WM + (erow % 16) + i * 16);
+        uint32_t vo[8];   // byte offsets of the unit's real columns; kNoLoad where absent
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            vo[e] = (WHOLE || (t0 + e >= 0 && t0 + e < nt)) ? (row * Nr + (uint32_t)(r0 + e)) * 2u : kNoLoad;
+        const uint32_t vu = (row * Nr + (uint32_t)r0) * 2u;
+        if constexpr (ADD) {
+            // slice column (c % D) * bnp + c / D, stepped along the unit
+            int res = r0 % D, quo = r0 / D;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t so = vo[e] == kNoLoad ? kNoLoad : (row * Np + (uint32_t)(res * bnp + quo)) * 4u;
+                x[e] += __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rS, (int)so, 0, 0));
+                const bool wrap = ++res == D;
+                res = wrap ? 0 : res;
+                quo += wrap ? 1 : 0;
+            }
+        }
+        if (bias) {
+            if constexpr (WHOLE) {
+                const uint4 b = ldg16(a.bias + r0);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += unpack_bf16(word_of(b, e >> 1), e & 1);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (vo[e] != kNoLoad) x[e] += bf16_to_f32(a.bias[r0 + e]);
+            }
+        }
+        if (grad) {
+            if constexpr (WHOLE) {
+                const uint4 h = bload16_stream(rH, vu, 0);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] *= gelu_grad(unpack_bf16(word_of(h, e >> 1), e & 1));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t h = __builtin_amdgcn_raw_buffer_load_b16(rH, (int)vo[e], 0, 0);
+                    x[e] *= gelu_grad(__uint_as_float(h << 16));
+                }
+            }
+        } else if (act) {
+            if (keep_h) {
+                if constexpr (WHOLE) {
+                    bstore16(rH, vu, make_uint4(pack_bf16(x[0], x[1]), pack_bf16(x[2], x[3]), pack_bf16(x[4], x[5]),
+                                                pack_bf16(x[6], x[7])));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        __builtin_amdgcn_raw_buffer_store_b16((unsigned short)f32_to_bf16(x[e]), rH, (int)vo[e], 0, 0);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = gelu(x[e]);
+        }
+        if constexpr (WHOLE) {
+            bstore16(rO, vu, make_uint4(pack_bf16(x[0], x[1]), pack_bf16(x[2], x[3]), pack_bf16(x[4], x[5]),
+                                        pack_bf16(x[6], x[7])));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                __builtin_amdgcn_raw_buffer_store_b16((unsigned short)f32_to_bf16(x[e]), rO, (int)vo[e], 0, 0);
+        }
+    };
+
+#pragma unroll
+    for (int i = 0; i < C::kSubM; ++i) {
+        float *ldsE = reinterpret_cast<float *>(smem) + (i & 1) * kElems;
+#pragma unroll
+        for (int j = 0; j < C::kSubN; ++j) {
+            const int col = wn0 + j * 16 + (lane & 15) + sh;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int er = (wave / C::kWGN) * 16 + (lane >> 4) * 4 + v;
+                ldsE[er * kPitch + col] = acc[i][j][v];
+            }
+        }
+        __syncthreads();
+        for (int w = tid; w < C::kEpiRows * n_whole; w += T)
+            unit(std::true_type{}, ldsE, w / n_whole, u_lo + w % n_whole, i);
+        // ragged units: unit 0 when shifted, then unit u_hi (all units when rows are unaligned)
+        for (int w = tid; w < C::kEpiRows * n_rag; w += T) {
+            const int k = w % n_rag;
+            const int u = vec ? (sh && k == 0 ? 0 : u_hi) : k;
+            unit(std::false_type{}, ldsE, w / n_rag, u, i);
         }
     }
 }

@@ -70,12 +70,19 @@ struct Gemm2Cfg {
 // first added to those of slice a.slice0 (read at the block-order place of
 // each column when a.unperm).  Component 2 alone under an output transpose needs no output
 // block per tile: its columns f = j*D + g take weight group f % D and row
-// f / D whatever block f falls in.
+// f / D whatever block f falls in.  The zero-padded forms (block-ordered
+// operands, gemm_epilogue_pad): ONLY = 4 component 1 adding the slice of
+// component 2 (run with ONLY = 1) under an output transpose, ONLY = 5 both
+// components, the second reading its own input copy a.in2 at the first's
+// places.
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY = 0>
 __global__ void __launch_bounds__(64 * WGM * WGN, 1)
 dyad_gemm_mfma2(GemmArgs a) {
     using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
     constexpr int T = C::kThreads;
+    // ONLY 1, 3 and 4 run component 1 alone; 4 and 5 are the zero-padded forms
+    static_assert(ONLY < 4 || (!IN_T && !OUT_T), "padded forms run on block-ordered operands");
+    constexpr bool kComp1Only = ONLY == 1 || ONLY == 3 || ONLY == 4;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::kLds];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -99,6 +106,8 @@ dyad_gemm_mfma2(GemmArgs a) {
     const int64_t rows_left = a.M - m0;
     const uint64_t a_bytes = (uint64_t)(rows_left < BM ? rows_left : BM) * (uint64_t)Kin * 2u;
     const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(a.in + m0 * a.Kin, (uint32_t)a_bytes);
+    // component 2's input: with ONLY == 5 its own block-ordered copy
+    const __amdgpu_buffer_rsrc_t rA2 = ONLY == 5 ? buffer_rsrc(a.in2 + m0 * a.Kin, (uint32_t)a_bytes) : rA;
     const uint32_t w_bytes = (uint32_t)(a.D * a.bn * a.bk * 2);
     const __amdgpu_buffer_rsrc_t rW1 = buffer_rsrc(a.W1, w_bytes);
     const __amdgpu_buffer_rsrc_t rW2 = buffer_rsrc(a.W2, w_bytes);
@@ -125,6 +134,7 @@ dyad_gemm_mfma2(GemmArgs a) {
         const int r = IN_T ? 0 : p / C::kRowChunks, rc = p % C::kRowChunks, row = rc >> 2, c = rc & 3;
         const uint32_t rowoff = (uint32_t)row * (uint32_t)Kin * 2u;
         if constexpr (IN_T) voA2[q] = rowoff + (uint32_t)(c * 8 * D) * 2u;            // span of 8 k x D residues
+        else if constexpr (ONLY == 5) voA2[q] = rowoff + (uint32_t)(g1 * bk + c * 8) * 2u;   // block g1 of in2
         else voA2[q] = rowoff + (uint32_t)(r * bk + c * 8) * 2u;                      // residue r's input block
         loA2[q] = (uint32_t)(C::kOffA2 + r * C::kSlab) + (uint32_t)lds_off(row, c) * 2u;
         if (!okA2[q]) voA2[q] = kNoLoad;
@@ -189,12 +199,12 @@ dyad_gemm_mfma2(GemmArgs a) {
             for (int q = 0; q < C::kQA1; ++q) ra1[q] = bload16(rA, voA1[q], kk * 2u);
         }
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQA2); ++q) {
+        for (int q = 0; q < (kComp1Only ? 0 : C::kQA2); ++q) {
             if constexpr (IN_T) {
 #pragma unroll
                 for (int d = 0; d < D; ++d) ra2[q][d] = bload16(rA, voA2[q] + d * 16u, kk * D * 2u);
             } else {
-                ra2[q][0] = bload16(rA, voA2[q], kk * 2u);
+                ra2[q][0] = bload16(rA2, voA2[q], kk * 2u);
             }
         }
         const uint32_t kb = W_T ? kk * (uint32_t)bn * 2u : kk * 2u;
@@ -203,7 +213,7 @@ dyad_gemm_mfma2(GemmArgs a) {
 #pragma unroll
             for (int d = 0; d < C::kVB1; ++d) rb1[q][d] = bload16(rW1, voB1[q] + d * 16u, kb);
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQB); ++q) rb2[q] = bload16(rW2, voB2[q], kb);
+        for (int q = 0; q < (kComp1Only ? 0 : C::kQB); ++q) rb2[q] = bload16(rW2, voB2[q], kb);
     };
 
     // ---- registers -> LDS stage buffer
@@ -212,7 +222,7 @@ dyad_gemm_mfma2(GemmArgs a) {
         for (int q = 0; q < (ONLY == 2 ? 0 : C::kQA1); ++q)
             if (C::kRowChunks % T == 0 || okA1[q]) *reinterpret_cast<uint4 *>(buf + loA1[q]) = ra1[q];
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQA2); ++q) {
+        for (int q = 0; q < (kComp1Only ? 0 : C::kQA2); ++q) {
             if (C::kUnitsA2 % T != 0 && !okA2[q]) continue;
             if constexpr (IN_T) {
                 uint4 span[D];
@@ -240,7 +250,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             }
         }
 #pragma unroll
-        for (int q = 0; q < (ONLY == 1 || ONLY == 3 ? 0 : C::kQB); ++q)
+        for (int q = 0; q < (kComp1Only ? 0 : C::kQB); ++q)
             if (C::kUnitsB % T == 0 || okB2[q]) *reinterpret_cast<uint4 *>(buf + loB2[q]) = rb2[q];
     };
 
@@ -268,7 +278,7 @@ dyad_gemm_mfma2(GemmArgs a) {
             }
         }
 #pragma unroll
-        for (int rr = 0; rr < (ONLY == 1 || ONLY == 3 ? 0 : C::kRPW); ++rr) {
+        for (int rr = 0; rr < (kComp1Only ? 0 : C::kRPW); ++rr) {
             const int r = OUT_T ? (wn0 + rr * C::kCPR) / C::kCPR : 0;
             const unsigned char *slab = buf + C::kOffA2 + r * C::kSlab;
 #pragma unroll
@@ -315,6 +325,8 @@ dyad_gemm_mfma2(GemmArgs a) {
     if constexpr (ONLY == 3)
         gemm_epilogue_as<C, BM, BN, D, OUT_T, false, true>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0,
                                                            split);
+    else if constexpr (ONLY >= 4)
+        gemm_epilogue_pad<C, BM, BN, ONLY == 4>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0);
     else
         gemm_epilogue<C, BM, BN, D, OUT_T>(a, smem, acc, m0, n0, rows_left, tid, lane, wave, wn0, split);
 }

@@ -32,6 +32,7 @@ hipError_t launch_mfma_gemm(const GemmPass &p, hipStream_t) {
     g_seen_bytes = sc ? sc->bytes : 0;
     return g_result;
 }
+hipError_t launch_padded_gemm(const GemmPass &p, hipStream_t) { ++g_launches; g_gemm = p; return g_result; }
 hipError_t launch_general_mfma_gemm(const GemmPass &p, hipStream_t) { ++g_launches; g_gemm = p; return g_result; }
 hipError_t launch_simt_gemm(const GemmPass &p, hipStream_t) { ++g_launches; g_gemm = p; return g_result; }
 bool mfma_dw_ok(const DwPass &) { return true; }

@@ -107,13 +107,42 @@ def test_backward_dw_rejects_and_workspace_size():
     assert dy.dyad_backward_dw(**dict(a, dW2=None)) == -1
     assert dy.dyad_backward_dw(**dict(a, X=FAKE + 1)) == -3
     assert dy.dyad_backward_dw(**dict(a, n_dyad=5, X=FAKE + 1)) == -3   # padded widths pass the shape check
-    # padded widths run on the general kernels, which split the tokens through
-    # the workspace: fp32 partials of dW1, dW2 and db per split
+    # padded widths in fp32 run on the general kernels, which split the tokens
+    # through the workspace: fp32 partials of dW1, dW2 and db per split
     per_split = 4 * (2 * 5 * 615 * 154 + 3072)
-    for dtype in (0, 1):
-        w5 = dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, dtype)
-        assert w5 > 0 and w5 % per_split == 0
+    w5 = dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 0)
+    assert w5 > 0 and w5 % per_split == 0
+    assert dy.dyad_dw_workspace_bytes(2, 768, 3072, 5, 16384, 1) == padded_dw_workspace(768, 3072, 5, 16384, True, True)
     assert dy.dyad_dw_workspace_bytes(9, 768, 3072, 4, 16384, 1) == 0
+
+
+def r256(b):
+    return (b + 255) // 256 * 256
+
+
+def padded_dw_workspace(n_in, n_out, D, M, in_t, out_t):
+    """Workspace of the zero-padded weight-gradient form, restated: blocks padded
+    to multiples of 64, the plain tile plan on them (first configuration whose
+    tile divides both padded blocks; token splits filling one round of workgroup
+    slots, each at least 8 stages of 32 tokens, a multiple of 64 tokens long),
+    then its fp32 partials, the copies of dZ and X (two each under a transpose)
+    and the padded dW1, dW2 and db."""
+    bi, bo = -(-n_in // D), -(-n_out // D)
+    bip, bop = -(-bi // 64) * 64, -(-bo // 64) * 64
+    configs = [(256, 256, 2, 4), (192, 256, 2, 4), (256, 192, 4, 2), (256, 128, 4, 2), (128, 256, 2, 4),
+               (128, 128, 2, 2), (128, 64, 2, 2), (64, 128, 2, 2), (64, 64, 2, 2), (128, 128, 4, 4)]
+    BJ, BK, WJ, WK = next(c for c in configs if bop % c[0] == 0 and bip % c[1] == 0)
+    tiles = 2 * D * (bop // BJ) * (bip // BK)
+    slots = 256 * (1 if WJ * WK >= 8 else 2)
+    splits = 1 if tiles >= slots else slots // tiles
+    splits = max(1, min(splits, M // 256))
+    tps = -(-M // splits)
+    tps = -(-tps // 64) * 64
+    splits = -(-M // tps)
+    part = 0 if splits == 1 else splits * (2 * D * bop * bip + D * bop) * 4
+    zb, xb = r256(M * D * bop * 2), r256(M * D * bip * 2)
+    wb = r256(D * bop * bip * 2)
+    return r256(part) + zb * (2 if out_t else 1) + xb * (2 if in_t else 1) + 2 * wb + D * bop * 2
 
 
 def test_dw_workspace_single_split():

@@ -251,6 +251,11 @@ PADDED = [  # (n_in, n_out, n_dyad, M)
     (768, 3072, 6, 300),   # blocks of 128 and 512
     (1536, 384, 6, 257),   # blocks of 256 and 64
     (384, 1536, 3, 2100),  # enough tokens for the de-interleaved forms of every pass
+    # from 512 tokens, shapes no fused tile takes run on zero-padded block copies:
+    (640, 1280, 5, 700),   # n_dyad 5 dividing both widths (blocks 128 / 256)
+    (896, 448, 7, 520),    # n_dyad 7 (blocks 128 / 64)
+    (776, 1544, 8, 600),   # blocks of 97 and 193, padded to 128 / 256
+    (768, 3072, 12, 512),  # n_dyad 12
 ]
 
 
