@@ -114,7 +114,7 @@ const ScratchScope *current_scratch();
 // once per device with hipGetSymbolAddress).
 hipError_t noalloc_scratch(void **out);
 hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s,
-                               bool perm_last = false);
+                               bool perm_last = false, int perm_from = 1 << 30);
 
 // out[n][g*bk + k] = in[n][k*D + g] for M token rows of D*bk bf16 values
 // (bk a multiple of 32, D a divisor of 64, 16-byte aligned rows).

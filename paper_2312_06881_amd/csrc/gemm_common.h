@@ -24,6 +24,10 @@ struct GemmArgs {
     // and the real output width and block size (Nout and bn are the padded ones)
     const uint16_t *in2;
     int64_t Nout_r, bn_r;
+    // tile order (fused-stage kernel): 0 token panels outer, so a workgroup's
+    // neighbours on its XCD share its input rows; 1 output columns outer, so
+    // they share its weights (few token panels, large weights)
+    int n_major;
 };
 
 // Epilogue of a BM x BN tile whose accumulators sit in the MFMA layout (wave w

@@ -90,8 +90,9 @@ dyad_gemm_mfma2(GemmArgs a) {
     // work item -> (tile, split), the splits of a tile next to each other
     const int item = xcd_tile(blockIdx.x, a.tiles_total * a.splits);
     const int tile = item / a.splits, split = item % a.splits;
-    const int64_t m0 = (int64_t)(tile / a.tiles_n) * BM;
-    const int n0 = (tile % a.tiles_n) * BN;        // first output column of the tile
+    const int tiles_m = a.tiles_total / a.tiles_n;
+    const int64_t m0 = (int64_t)(a.n_major ? tile % tiles_m : tile / a.tiles_n) * BM;
+    const int n0 = (a.n_major ? tile / tiles_m : tile % a.tiles_n) * BN;   // first output column of the tile
     const int bk = (int)a.bk, bn = (int)a.bn, Kin = (int)a.Kin;
     const int g1 = n0 / bn;                        // output block = BlockDiag group
     const int jb = n0 - g1 * bn;                   // first BlockDiag weight row / column

@@ -56,7 +56,7 @@ inline bool gemm_split_ws(const GemmPass &p, int splits, hipStream_t s, GemmArgs
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int PF = 1, bool GELU_IN = false>
 hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
     using C = GemmCfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
-    GemmArgs a;
+    GemmArgs a{};
     // buffer offsets are 32-bit: one token panel of the input and of the output,
     // and one weight tensor, must fit
     if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 2 >= ((int64_t)1 << 31) ||
@@ -89,7 +89,7 @@ hipError_t launch_tile(const GemmPass &p, hipStream_t s) {
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T>
 hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
     using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
-    GemmArgs a;
+    GemmArgs a{};
     if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 2 >= ((int64_t)1 << 31) ||
         2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
         return hipErrorNotSupported;
@@ -119,9 +119,9 @@ hipError_t launch_tile2(const GemmPass &p, hipStream_t s) {
 // into the pass's output with its epilogue, adding that slice (at the
 // block-order place of each column with `unperm`).
 template <int BM, int BN, int WGM, int WGN, int D, bool IN_T, bool OUT_T, bool W_T, int ONLY>
-hipError_t launch_component(const GemmPass &p, float *part, int slice, bool unperm, hipStream_t s) {
+hipError_t launch_component(const GemmPass &p, float *part, int slice, bool unperm, hipStream_t s, int splits = 1) {
     using C = Gemm2Cfg<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T>;
-    GemmArgs a;
+    GemmArgs a{};
     if ((int64_t)BM * p.Kin * 2 >= ((int64_t)1 << 31) || (int64_t)BM * p.Nout * 4 >= ((int64_t)1 << 31) ||
         2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31))
         return hipErrorNotSupported;
@@ -143,8 +143,13 @@ hipError_t launch_component(const GemmPass &p, float *part, int slice, bool unpe
     if (tiles_m * tiles_n >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     a.tiles_n = (int)tiles_n;
     a.tiles_total = (int)(tiles_m * tiles_n);
-    a.part = part; a.splits = 1; a.slice0 = slice; a.unperm = unperm;
-    dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, ONLY><<<a.tiles_total, C::kThreads, 0, s>>>(a);
+    // split s of the reduction (ONLY = 1 or 2) writes slice `slice` + s
+    if (splits < 1 || (p.bk / kStageK) % splits != 0 || (splits > 1 && ONLY > 2)) return hipErrorNotSupported;
+    a.part = part; a.splits = splits; a.slice0 = slice; a.unperm = unperm;
+    // a few token panels over many weight tiles: the panels of one weight tile
+    // run next to each other (on one XCD), which then reads those weights once
+    a.n_major = tiles_m <= 8 && tiles_n >= 64;
+    dyad_gemm_mfma2<BM, BN, WGM, WGN, D, IN_T, OUT_T, W_T, ONLY><<<a.tiles_total * splits, C::kThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 
@@ -247,9 +252,23 @@ hipError_t launch_components(const GemmPass &p, hipStream_t s) {
 // (column g*bn + j for output column j*D + g) under an output transpose.  The
 // tokens run in chunks that keep the workspace (slice and de-interleaved
 // input) within 2 GiB.
+//
+// A batch whose tiles give each CU at most one workgroup, over a reduction of
+// at least 1024 (256 tokens of the wide layer: 256 tiles of 64 x 128 over
+// 2048) splits the reduction of both components into S parts, each its own
+// fp32 slice, so that every CU runs several workgroups with a shorter loop;
+// the split reduction then adds component 1's slices and component 2's (read
+// at the block-order place under an output transpose) in order and applies
+// the epilogue.  Measured there: fc1 input gradient 93 -> 80 µs, fc2
+// forward 87 -> 81 µs; over reductions of 512 (fc1 forward, fc2 input
+// gradient, whose outputs are 4x wider) the slices cost more than the split
+// saves (65 -> 104 µs).
 template <int BM, int BN, int WGM, int WGN, int D, bool W_T>
 hipError_t launch_permuted_as(const GemmPass &p, bool in_t, bool out_t, hipStream_t s) {
-    const size_t per_tok = (in_t ? (size_t)p.Kin * 2 : 0) + (size_t)p.Nout * sizeof(float);
+    const int64_t tiles = ((p.M + BM - 1) / BM) * (p.Nout / BN);
+    int S = 1;
+    while (tiles * S < 512 && S < 4 && (p.bk / kStageK) % (2 * S) == 0 && p.bk / kStageK / (2 * S) >= 16) S *= 2;
+    const size_t per_tok = (in_t ? (size_t)p.Kin * 2 : 0) + (size_t)(S > 1 ? 2 * S : 1) * p.Nout * sizeof(float);
     const size_t cap = (size_t)2 << 30;
     int64_t mc = (int64_t)(cap / per_tok);
     if (mc >= p.M) mc = p.M;
@@ -261,7 +280,7 @@ hipError_t launch_permuted_as(const GemmPass &p, bool in_t, bool out_t, hipStrea
         return hipErrorNotSupported;
     }
     float *part = static_cast<float *>(ws);
-    uint16_t *xp = reinterpret_cast<uint16_t *>(part + mc * p.Nout);
+    uint16_t *xp = reinterpret_cast<uint16_t *>(part + (S > 1 ? 2 * S : 1) * mc * p.Nout);
     hipError_t e = hipSuccess;
     for (int64_t m0 = 0; m0 < p.M && e == hipSuccess; m0 += mc) {
         GemmPass c = p;
@@ -275,6 +294,13 @@ hipError_t launch_permuted_as(const GemmPass &p, bool in_t, bool out_t, hipStrea
         if (in_t) {
             e = launch_deinterleave(static_cast<const uint16_t *>(c.in), xp, c.M, p.bk, D, s);
             c2.in = xp;
+        }
+        if (S > 1) {
+            // slices 0 .. S-1: component 1, S .. 2S-1: component 2 (block order)
+            if (e == hipSuccess) e = launch_component<BM, BN, WGM, WGN, D, false, false, W_T, 1>(c, part, 0, false, s, S);
+            if (e == hipSuccess) e = launch_component<BM, BN, WGM, WGN, D, false, false, W_T, 1>(c2, part, S, false, s, S);
+            if (e == hipSuccess) e = launch_split_reduce(c, part, 2 * S, s, false, out_t ? S : 2 * S);
+            continue;
         }
         if (e == hipSuccess) e = launch_component<BM, BN, WGM, WGN, D, false, false, W_T, 1>(c2, part, 0, false, s);
         if (e == hipSuccess) e = launch_component<BM, BN, WGM, WGN, D, false, false, W_T, 3>(c, part, 0, out_t, s);

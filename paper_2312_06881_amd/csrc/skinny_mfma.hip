@@ -254,10 +254,10 @@ __global__ void __launch_bounds__(64 * kSkWaves) skinny_part_kernel(SkArgs a) {
 }
 
 // out[n][f] = epilogue(sum of the slices, in slice order); 8 columns per thread.
-// PERM: the last slice holds its sums in block order, output column j*D + g at
-// column g*bn + j, and is read there.
+// PERM: slices perm_from .. slices-1 hold their sums in block order, output
+// column j*D + g at column g*bn + j, and are read there.
 template <bool PERM>
-__global__ void __launch_bounds__(256) skinny_reduce_kernel(GemmPass p, const float *part, int slices) {
+__global__ void __launch_bounds__(256) skinny_reduce_kernel(GemmPass p, const float *part, int slices, int perm_from) {
     const int64_t per_row = p.Nout / 8;
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (idx >= p.M * per_row) return;
@@ -271,7 +271,7 @@ __global__ void __launch_bounds__(256) skinny_reduce_kernel(GemmPass p, const fl
         for (int v = 0; v < 4; ++v) { x[v] = lo[v]; x[4 + v] = hi[v]; }
     }
     for (int s = 1; s < slices; ++s) {
-        if (PERM && s == slices - 1) {
+        if (PERM && s >= perm_from) {
             const float *row = part + s * stride + n * p.Nout;
             const int D = (int)p.D, bn = (int)p.bn;
 #pragma unroll
@@ -487,14 +487,17 @@ hipError_t split_workspace(hipStream_t s, size_t bytes, void **out) {
     return hipSuccess;
 }
 
-hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s, bool perm_last) {
+hipError_t launch_split_reduce(const GemmPass &p, const float *part, int slices, hipStream_t s, bool perm_last,
+                               int perm_from) {
     if (p.Nout % 8 != 0) return hipErrorNotSupported;
     const int64_t threads = p.M * (p.Nout / 8);
     const unsigned blocks = (unsigned)((threads + 255) / 256);
-    if (perm_last)
-        skinny_reduce_kernel<true><<<blocks, 256, 0, s>>>(p, part, slices);
+    if (perm_last) perm_from = slices - 1;
+    if (perm_from < 1) perm_from = 1;   // slice 0 is read in output order
+    if (perm_from < slices)
+        skinny_reduce_kernel<true><<<blocks, 256, 0, s>>>(p, part, slices, perm_from);
     else
-        skinny_reduce_kernel<false><<<blocks, 256, 0, s>>>(p, part, slices);
+        skinny_reduce_kernel<false><<<blocks, 256, 0, s>>>(p, part, slices, slices);
     return hipGetLastError();
 }
 

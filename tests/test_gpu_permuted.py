@@ -181,3 +181,29 @@ def test_wide_blocks_1030_tokens_sampled(variant):
     rdx = oracle.backward_dx(variant, n_in, n_out, D, L.dZ[rows].to(torch.float64).numpy(), W1, W2)
     assert_close(y[rows], ry, "bf16", "Y rows")
     assert_close(dx[rows], rdx, "bf16", "dX rows")
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("layer", [(8192, 32768), (32768, 8192)], ids=["fc1", "fc2"])
+def test_wide_layer_256_tokens_split_sampled(layer, variant):
+    """The wide layer 8192 <-> 32768 at n_dyad 16 with 256 tokens: the passes
+    whose reduction blocks are 2048 wide (fc2 forward, fc1 input gradient)
+    split the reduction of both components in two, each part its own fp32
+    slice, added in order by the split reduction.  Forward with GELU, input
+    gradient with GELU', on sampled rows."""
+    n_in, n_out = layer
+    D, M = 16, 256
+    banner("permuted_split256", layer, variant)
+    L = layer_inputs(n_in, n_out, D, M, "bf16", seed_offset=11)
+    y, h = dy.forward(gpu(L.X), gpu(L.W1), gpu(L.W2), gpu(L.bias), variant=variant, act="gelu", stash_h=True)
+    dx = dy.backward_dx(gpu(L.dZ), gpu(L.W1), gpu(L.W2), variant=variant, act_in="gelu", h_in=gpu(L.H_in))
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 63, 64, 127, 128, 200, M - 1])
+    W1, W2 = L.f64("W1"), L.f64("W2")
+    ry, rh = oracle.forward(variant, n_in, n_out, D, L.X[rows].to(torch.float64).numpy(), W1, W2, L.f64("bias"),
+                            act=oracle.ACT_GELU, want_h=True)
+    rdx = oracle.backward_dx(variant, n_in, n_out, D, L.dZ[rows].to(torch.float64).numpy(), W1, W2,
+                             act_in=oracle.ACT_GELU, H_in=L.H_in[rows].to(torch.float64).numpy())
+    assert_close(y[rows], ry, "bf16", "Y rows")
+    assert_close(h[rows], rh, "bf16", "H rows")
+    assert_close(dx[rows], rdx, "bf16", "dX rows")
