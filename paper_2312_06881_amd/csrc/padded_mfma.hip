@@ -4,26 +4,30 @@
 
 namespace dyad {
 
-// One token row per workgroup: the row comes into LDS with 16-byte loads
-// (W % 8 == 0), then each thread assembles 8 consecutive padded columns of
-// an output from LDS and stores them as 16 bytes (bp % 8 == 0, so the 8 lie
-// in one block).
-__global__ void __launch_bounds__(256) pad_rows_kernel(const uint16_t *src, int W, int D, int b, int bp,
-                                                       uint16_t *dst1, uint16_t *dst2) {
+// R token rows per workgroup (R * W about 8192 elements, so a narrow row
+// does not leave most of the workgroup idle): the rows come into LDS with
+// 16-byte loads (W % 8 == 0), then each thread assembles 8 consecutive
+// padded columns of an output row from LDS and stores them as 16 bytes
+// (bp % 8 == 0, so the 8 lie in one block).
+__global__ void __launch_bounds__(256) pad_rows_kernel(const uint16_t *src, int64_t M, int W, int R, int D, int b,
+                                                       int bp, uint16_t *dst1, uint16_t *dst2) {
     extern __shared__ u32x4_t row_lds[];
-    const int64_t m = blockIdx.x;
-    const u32x4_t *s = reinterpret_cast<const u32x4_t *>(src + m * W);
-    for (int v = threadIdx.x; v < W / 8; v += 256) row_lds[v] = __builtin_nontemporal_load(s + v);
+    const int64_t m0 = (int64_t)blockIdx.x * R;
+    const int rows = M - m0 < R ? (int)(M - m0) : R;
+    const int vpr = W / 8;                         // 16-byte vectors per row
+    const u32x4_t *s = reinterpret_cast<const u32x4_t *>(src + m0 * W);
+    for (int v = threadIdx.x; v < rows * vpr; v += 256) row_lds[v] = __builtin_nontemporal_load(s + v);
     __syncthreads();
-    const uint16_t *r = reinterpret_cast<const uint16_t *>(row_lds);
-    const int units = D * bp / 8;
+    const int units = D * bp / 8;                  // 8-column units per output row
     const int64_t Wp = (int64_t)D * bp;
-    for (int u = threadIdx.x; u < units; u += 256) {
-        const int g = (8 * u) / bp, k0 = 8 * u - g * bp;
-        for (int o = 0; o < 2; ++o) {
-            uint16_t *dst = o == 0 ? dst1 : dst2;
-            if (!dst) continue;
-            uint32_t w[4];
+    for (int o = 0; o < 2; ++o) {
+        uint16_t *dst = o == 0 ? dst1 : dst2;
+        if (!dst) continue;
+        for (int w = threadIdx.x; w < rows * units; w += 256) {
+            const int rr = w / units, u = w - rr * units;
+            const uint16_t *r = reinterpret_cast<const uint16_t *>(row_lds + rr * vpr);
+            const int g = (8 * u) / bp, k0 = 8 * u - g * bp;
+            uint32_t q[4];
 #pragma unroll
             for (int h = 0; h < 4; ++h) {
                 uint32_t pair = 0;
@@ -34,9 +38,9 @@ __global__ void __launch_bounds__(256) pad_rows_kernel(const uint16_t *src, int 
                     const uint32_t v = (k < b && col < W) ? (uint32_t)r[col] : 0u;
                     pair |= v << (16 * e);
                 }
-                w[h] = pair;
+                q[h] = pair;
             }
-            *reinterpret_cast<uint4 *>(dst + m * Wp + 8 * u) = make_uint4(w[0], w[1], w[2], w[3]);
+            *reinterpret_cast<uint4 *>(dst + (m0 + rr) * Wp + 8 * u) = make_uint4(q[0], q[1], q[2], q[3]);
         }
     }
 }
@@ -46,8 +50,11 @@ hipError_t launch_pad_rows(const uint16_t *src, int64_t M, int64_t W, int D, int
     if (W % 8 != 0 || W > kPadMaxRow || bp % 8 != 0 || b > bp || M < 0 || (!dst1 && !dst2))
         return hipErrorNotSupported;
     if (M == 0) return hipSuccess;
-    if (M >= ((int64_t)1 << 31)) return hipErrorNotSupported;
-    pad_rows_kernel<<<(unsigned)M, 256, (size_t)W * 2, s>>>(src, (int)W, D, (int)b, (int)bp, dst1, dst2);
+    const int R = W >= 8192 ? 1 : (int)(8192 / W);   // at most 16 KB of LDS
+    const int64_t blocks = (M + R - 1) / R;
+    if (blocks >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+    pad_rows_kernel<<<(unsigned)blocks, 256, (size_t)R * W * 2, s>>>(src, M, (int)W, R, D, (int)b, (int)bp, dst1,
+                                                                      dst2);
     return hipGetLastError();
 }
 
