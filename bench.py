@@ -523,6 +523,7 @@ def summarize_pmc(args, call, fetch_dir, write_dir):
     fetch = f_kib * 1024 * f_scale
     write = w_kib * 1024 * w_scale
     path = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+    wl = "" if args.workload == "opt125m_ff" else f" --workload {args.workload}"
     rec = {}
     if os.path.exists(path):
         rec = json.load(open(path))
@@ -533,8 +534,8 @@ def summarize_pmc(args, call, fetch_dir, write_dir):
                           "write_raw_kib": round(w_kib, 1), "fetch_scale": round(f_scale, 4),
                           "write_scale": round(w_scale, 4), "launches": [n_f, n_w],
                           "commands": [f"rocprofv3 --pmc {c} --output-format csv -d <dir>/{c} -o run -- "
-                                       f"python -u bench.py --only {call} --steps 5" for c in ("FETCH_SIZE", "WRITE_SIZE")]
-                          + [f"python bench.py --summarize-pmc {call} <dir>/FETCH_SIZE <dir>/WRITE_SIZE"]}
+                                       f"python -u bench.py{wl} --only {call} --steps 5" for c in ("FETCH_SIZE", "WRITE_SIZE")]
+                          + [f"python bench.py{wl} --summarize-pmc {call} <dir>/FETCH_SIZE <dir>/WRITE_SIZE"]}
     os.makedirs(os.path.dirname(path), exist_ok=True)
     with open(path, "w") as fh:
         json.dump(rec, fh, indent=1, sort_keys=True)
@@ -544,6 +545,19 @@ def summarize_pmc(args, call, fetch_dir, write_dir):
 SQ_COUNTERS = ("SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES "
                "SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE")
 N_SIMD, N_XCD = 1024, 8   # MI355X: 256 CUs x 4 SIMDs, in 8 XCDs
+
+
+def _kernel_short(name):
+    """A kernel's name without its argument list and return type (keeps '(anonymous namespace)')."""
+    name = name.strip()
+    if name.endswith(")"):
+        depth = 0
+        for i in range(len(name) - 1, -1, -1):
+            depth += {")": 1, "(": -1}.get(name[i], 0)
+            if depth == 0:
+                name = name[:i]
+                break
+    return name[5:] if name.startswith("void ") else name
 
 
 def _launch_sums(rows, counters):
@@ -560,7 +574,7 @@ def _launch_sums(rows, counters):
             continue
         if r["Counter_Name"] in counters:
             cur[r["Counter_Name"]] = cur.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
-            kernels.add(r["Kernel_Name"].split("(")[0])
+            kernels.add(_kernel_short(r["Kernel_Name"]))
     if cur:
         launches.append(cur)
     copy = {}
@@ -613,7 +627,7 @@ def summarize_counters(args, root):
         for call, n, cyc, mf, wt, fl, fb, wb, ks in lines:
             fh.write(f"{call:12s} {n:8d} {cyc:11.0f} {mf:9.3f} {wt:6.3f} {fl / 1e9:10.2f} "
                      f"{'-' if fb is None else f'{fb / 1e6:9.1f}':>9s} {'-' if wb is None else f'{wb / 1e6:9.1f}':>9s}  "
-                     f"{'; '.join(k.replace('void dyad::', '') for k in ks)}\n")
+                     f"{'; '.join(k.replace('dyad::', '').replace('(anonymous namespace)::', '') for k in ks)}\n")
     print(open(path).read())
 
 
