@@ -45,13 +45,15 @@ def run(fn, variant, L, act, stream):
 
 
 # (n_in, n_out, n_dyad, [M of the first call, M of the second]): small batches on the
-# split-reduction paths (buffers of a few MiB), and n_dyad 16 with 64-column blocks at a
-# batch whose two fp32 component slices (512 MiB) exceed the array
+# split-reduction paths (buffers of a few MiB), n_dyad 16 with 64-column blocks at a
+# batch whose two fp32 component slices (512 MiB) exceed the array, and zero-padded
+# blocks (n_dyad 5) on the padded forms, whose copies and slice (15 MiB) fit it
 CASES = [
     (8192, 8192, 16, (32, 16)),
     (768, 3072, 4, (32, 9)),
     (3072, 768, 4, (200, 17)),
     (4096, 1024, 16, (16384, 2100)),
+    (768, 3072, 5, (1000, 600)),
 ]
 
 
