@@ -29,8 +29,10 @@
  *
  * Ownership and ordering: the caller allocates and owns every buffer, the
  * dW workspace included; dyad_backward_dw allocates nothing (its fp32 partial
- * sums and, at n_dyad 8 / 16 with large batches, the de-interleaved copies of
- * dZ and / or X all live in the workspace the caller passes).
+ * sums, the de-interleaved copies of dZ and / or X at n_dyad 3, 6, 8 and 16
+ * with large batches, and for shapes the fused tiles refuse the zero-padded
+ * block copies of dZ and X and the padded gradients all live in the
+ * workspace the caller passes).
  * dyad_forward and dyad_backward_dx are the one bounded departure from
  * "caller owns everything": they may keep intermediates in a library-owned
  * device buffer, one per (device, stream), taken in stream order from a
@@ -38,8 +40,10 @@
  * stream order when a later call needs more, and kept until the process
  * ends.  It holds the fp32 partial sums of a split reduction (small batches,
  * few output tiles; a few slices of M x n_out fp32, at most 2 GiB) and, at
- * n_dyad 8 / 16 with large batches, a de-interleaved copy of the input and
- * one fp32 slice of the output (at most 2 GiB; the tokens are taken in chunks
+ * n_dyad 3, 6, 8 and 16 with large batches, a de-interleaved copy of the
+ * input and fp32 slices of the output; for shapes the fused tiles refuse
+ * (from 512 tokens), zero-padded block copies of the input and the weights
+ * and one fp32 slice (each form within 2 GiB; the tokens are taken in chunks
  * beyond that).  Calls on one stream share it in stream order; calls on
  * different streams never share it.  While the stream is being captured into
  * a graph the buffer is never allocated or regrown; when it cannot be had
