@@ -550,10 +550,10 @@ bool skinny_ok(const GemmPass &p) {
     if (p.M > 32 && !(p.w_t && p.out_t && p.D >= 16)) return false;
     if (p.Kin != p.D * p.bk || p.Nout != p.D * p.bn) return false;
     // where the large-batch form (de-interleaved input, per-block GEMMs) pays,
-    // it goes first, except without an input transpose and with reduction
-    // blocks above 512 (wide layer 8192 -> 32768 at 256 tokens: Dyad-IT fc1
-    // input gradient 70 us here against 85 there; the DT one 167 against 89)
-    if (p.M > 32 && (p.in_t || p.bk <= 512) && permuted_pays((int)p.D, p.out_t, p.w_t, p.M, p.bk)) return false;
+    // it goes first (wide layer 8192 -> 32768 at 256 tokens: Dyad-IT fc1 input
+    // gradient 49 us there against 73 here, with its split reduction and
+    // weight-major tile order; the DT one 56 against 167)
+    if (p.M > 32 && permuted_pays((int)p.D, p.out_t, p.w_t, p.M, p.bk)) return false;
     // 32-bit buffer offsets: the weights and the input panel
     if (2 * p.D * p.bn * p.bk >= ((int64_t)1 << 31) || 2 * p.M * p.Kin >= ((int64_t)1 << 31)) return false;
     if (p.bn % 128 != 0) return false;

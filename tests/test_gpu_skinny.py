@@ -112,7 +112,7 @@ def test_forward_and_dx_up_to_256_tokens(shape, variant, M):
     """Batches of 33-256 tokens (GELU forward with stash, GELU' input gradient).
     At n_dyad 16 the output-transposed input gradients take the small-batch
     path, its waves splitting the tokens 32 at a time and looping over chunks
-    of the reduction (at 256 tokens with reduction blocks of 512, the
+    of the reduction (at 256 tokens with reduction blocks of 512 or more, the
     large-batch path instead); the other passes run on the tiled kernels."""
     n_in, n_out, D = shape
     banner("mid", shape, variant, M)
