@@ -413,6 +413,16 @@ def test_full_size_odd_dyad_sampled(D, variant):
         check_full_layer(n_in, n_out, D, OPT125M.M, variant, fa, da, seed_offset=li)
 
 
+# The zero-padded forms take the tokens in chunks that keep their copies and
+# slice within 2 GiB: with 16360 outputs at n_dyad 5 (blocks of 154 / 3272,
+# padded to 160 / 3328) a chunk under an output transpose holds about 31500
+# tokens, so 40000 tokens run as two, the second ragged.
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_padded_forms_token_chunks_sampled(variant):
+    banner("padded chunks", variant)
+    check_full_layer(768, 16360, 5, 40000, variant, "gelu", "none", seed_offset=3)
+
+
 @pytest.mark.parametrize("variant", VARIANTS)
 @pytest.mark.parametrize("shape", [(768, 3072, 4, 5000), (3072, 768, 4, 3001), (1024, 1024, 16, 2049)],
                          ids=case_id)
